@@ -1,0 +1,195 @@
+"""CPU oracle for the quantized selective-state update (test infrastructure).
+
+Only the tests, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package. It is a plain, slow statement of what the
+GPU library computes (see ``ssmq_oracle.c`` for the definitions and the
+floating-point order) and shares no code with it.
+
+Formats: "fp16", "bf16", "e4m3" (OCP E4M3FN with an fp32 group scale), "fp32"
+(unrounded). Rules: "rtn", "sr", "weyl".
+
+Parity status: every function here is pinned by tests under ``tests/`` that use
+what the paper and the mathematics fix (worked values, closed forms, exact
+rational evaluation, library casts). The device ``exp`` and the quality of the
+stochastic-rounding stream beyond its moments are not pinned.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build_oracle
+
+FORMATS = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3}
+RULES = {"rtn": 0, "sr": 1, "weyl": 2}
+CODE_DTYPE = {"fp16": np.uint16, "bf16": np.uint16, "e4m3": np.uint8, "fp32": np.uint32}
+
+_lib = None
+
+_u32 = ctypes.c_uint32
+_u64 = ctypes.c_uint64
+_i64 = ctypes.c_int64
+_int = ctypes.c_int
+_vp = ctypes.c_void_p
+
+
+def lib() -> ctypes.CDLL:
+    """Load the oracle library, building it first only if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(build_oracle.LIBRARY):
+        build_oracle.build()
+    L = ctypes.CDLL(build_oracle.LIBRARY)
+    L.orc_weyl_constants.argtypes = [ctypes.POINTER(_u32)]
+    L.orc_weyl_constants.restype = None
+    L.orc_fmix32.argtypes = [_u32]
+    L.orc_fmix32.restype = _u32
+    L.orc_grid.argtypes = [_int, _vp, _vp, _int]
+    L.orc_grid.restype = _int
+    L.orc_decode.argtypes = [_int, _u32]
+    L.orc_decode.restype = ctypes.c_double
+    L.orc_code_rank.argtypes = [_int, _u32]
+    L.orc_code_rank.restype = _int
+    L.orc_round.argtypes = [_int, _int, ctypes.c_float, _u32]
+    L.orc_round.restype = _u32
+    L.orc_round_array.argtypes = [_int, _int, _i64, _vp, _vp, _vp]
+    L.orc_round_array.restype = None
+    L.orc_threshold.argtypes = [_int, _u32, _u32, _u32, _u64, _u64]
+    L.orc_threshold.restype = _u32
+    L.orc_dither_fill.argtypes = [_int, _u32, _u32, _u32, _u64, _i64, _u64, _vp]
+    L.orc_dither_fill.restype = None
+    L.orc_requantize.argtypes = [_int, _int, _u32, _u32, _u32, _u64, _u64, _i64, _i64, _vp, _vp,
+                                 _vp]
+    L.orc_requantize.restype = _int
+    L.orc_state_update.argtypes = [_int, _int, _u32, _u32, _u32, _u64, _u64, _i64, _i64, _i64,
+                                   _i64, _i64, _i64, _int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                   _vp, _vp]
+    L.orc_state_update.restype = _int
+    _lib = L
+    return L
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(_vp)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def weyl_constants() -> dict:
+    """The integer constants of the Weyl accumulator (A, B, L, S, Phi)."""
+    out = (_u32 * 5)()
+    lib().orc_weyl_constants(out)
+    return dict(zip(("A", "B", "L", "S", "PHI"), [int(v) for v in out]))
+
+
+def fmix32(h: int) -> int:
+    return int(lib().orc_fmix32(h & 0xFFFFFFFF))
+
+
+def grid(fmt: str):
+    """Sorted finite value set of a format and the code of each value."""
+    f = FORMATS[fmt]
+    n = lib().orc_grid(f, None, None, 0)
+    vals = np.empty(n, np.float64)
+    codes = np.empty(n, np.uint32)
+    lib().orc_grid(f, _ptr(vals), _ptr(codes), n)
+    return vals, codes
+
+
+def decode(fmt: str, codes) -> np.ndarray:
+    """Value of each code (no scale) as float64."""
+    f = FORMATS[fmt]
+    c = np.asarray(codes).astype(np.uint32).ravel()
+    return np.array([lib().orc_decode(f, int(v)) for v in c], np.float64).reshape(np.shape(codes))
+
+
+def code_rank(fmt: str, codes) -> np.ndarray:
+    """Position of each code in value order (both zeros share one position)."""
+    f = FORMATS[fmt]
+    c = np.asarray(codes).astype(np.uint32).ravel()
+    return np.array([lib().orc_code_rank(f, int(v)) for v in c], np.int64).reshape(np.shape(codes))
+
+
+def round_values(fmt: str, rule: str, x, U24=None) -> np.ndarray:
+    """Round fp32 values with given 24-bit thresholds; returns codes (uint32)."""
+    x = _c(x, np.float32).ravel()
+    U = None if U24 is None else _c(U24, np.uint32).ravel()
+    out = np.empty(x.size, np.uint32)
+    lib().orc_round_array(FORMATS[fmt], RULES[rule], x.size, _ptr(x), _ptr(U), _ptr(out))
+    return out
+
+
+def thresholds(rule: str, seed: int, layer: int, step: int, entry_base: int, n: int,
+               block: int) -> np.ndarray:
+    """The 24-bit threshold of entries entry_base .. entry_base + n - 1."""
+    out = np.empty(n, np.uint32)
+    lib().orc_dither_fill(RULES[rule], seed & 0xFFFFFFFF, layer & 0xFFFFFFFF, step & 0xFFFFFFFF,
+                          entry_base, n, block, _ptr(out))
+    return out
+
+
+def requantize(fmt: str, rule: str, h, *, seed=0, layer=0, step=0, entry_base=0, block=16,
+               group=0):
+    """Codes (and E4M3 group scales) for fp32 values h."""
+    h = _c(h, np.float32).ravel()
+    codes = np.zeros(h.size, CODE_DTYPE[fmt])
+    scale = None
+    if fmt == "e4m3":
+        if group <= 0:
+            raise ValueError("e4m3 needs a positive group")
+        scale = np.zeros(h.size // group, np.float32)
+    rc = lib().orc_requantize(FORMATS[fmt], RULES[rule], seed & 0xFFFFFFFF, layer & 0xFFFFFFFF,
+                              step & 0xFFFFFFFF, entry_base, block, h.size, group, _ptr(h),
+                              _ptr(codes), _ptr(scale))
+    if rc != 0:
+        raise ValueError("oracle requantize rejected its arguments")
+    return codes, scale
+
+
+def state_update(fmt: str, rule: str, state, scale, x, dt, A, B, C, D, *, seed=0, layer=0,
+                 step=0, entry_base=0, block=16, group=0, a_per_state=None):
+    """One fused step. state has shape [batch, nheads, headdim, dstate] (codes).
+
+    Returns (new_state, new_scale, y (float64), h_new (fp32 pre-rounding)).
+    """
+    state = np.array(state, dtype=CODE_DTYPE[fmt], copy=True, order="C")
+    batch, nheads, headdim, dstate = state.shape
+    B = _c(B, np.float32)
+    ngroups = B.shape[1]
+    A = _c(A, np.float32)
+    if a_per_state is None:
+        a_per_state = 1 if A.ndim == 2 else 0
+    sc = None
+    if fmt == "e4m3":
+        sc = np.array(scale, dtype=np.float32, copy=True).ravel()
+    x = _c(x, np.float32)
+    dt = _c(dt, np.float32)
+    C = _c(C, np.float32)
+    D = None if D is None else _c(D, np.float32)
+    y = np.zeros((batch, nheads, headdim), np.float64)
+    hnew = np.zeros(state.shape, np.float32)
+    rc = lib().orc_state_update(FORMATS[fmt], RULES[rule], seed & 0xFFFFFFFF, layer & 0xFFFFFFFF,
+                                step & 0xFFFFFFFF, entry_base, block, group, batch, nheads,
+                                headdim, dstate, ngroups, a_per_state, _ptr(state), _ptr(sc),
+                                _ptr(x), _ptr(dt), _ptr(A), _ptr(B), _ptr(C), _ptr(D), _ptr(y),
+                                _ptr(hnew))
+    if rc != 0:
+        raise ValueError("oracle state_update rejected its arguments")
+    return state, sc, y, hnew
+
+
+def dequantize(fmt: str, codes, scale=None, group=0) -> np.ndarray:
+    """fp32 values of stored codes (E4M3: times the group scale, one fp32 product)."""
+    codes = np.asarray(codes)
+    if fmt == "fp32":
+        return codes.astype(np.uint32).view(np.float32).astype(np.float32)
+    v = decode(fmt, codes).astype(np.float32).ravel()
+    if fmt == "e4m3":
+        s = np.repeat(np.asarray(scale, np.float32).ravel(), group)
+        v = (v * s).astype(np.float32)
+    return v.reshape(codes.shape)

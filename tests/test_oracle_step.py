@@ -1,0 +1,253 @@
+"""Pins of the oracle's fused state update (CPU only).
+
+Expected values come from Section 3 (Lemma "Write erasure", Proposition 1,
+Corollary 1, Lemma "Per-write noise"), Appendix A (proofs, the decay bound)
+and from an independent float64 evaluation of the recurrence of Section 2,
+eq. (rec), in the Mamba-2 / Mamba-1 form of Appendix B ("Runners").
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import discrepancy as dsc
+from paper_2609_39185_amd import workloads as wl
+
+TWO24 = 1 << 24
+
+
+def _inputs(family, batch, nheads, headdim, dstate, ngroups, seed):
+    A, D = wl.layer_params(family, nheads, dstate, seed)
+    x, dt, B, C = wl.step_inputs(batch, nheads, headdim, dstate, ngroups, seed)
+    return {k: v.numpy() for k, v in dict(A=A, D=D, x=x, dt=dt, B=B, C=C).items()}
+
+
+@pytest.mark.parametrize("family,shape", [("mamba2", (2, 6, 8, 32, 2)), ("mamba1", (3, 40, 1, 16, 1))])
+def test_fp32_step_is_the_recurrence(orc, family, shape):
+    """Unrounded (fp32) step == exp(dt A) h + dt x B and y = C h + D x (float64 reference)."""
+    batch, nheads, headdim, dstate, ngroups = shape
+    p = _inputs(family, *shape, seed=11)
+    h0 = np.random.default_rng(3).standard_normal((batch, nheads, headdim, dstate)).astype(np.float32)
+    codes = h0.view(np.uint32)
+    new, _, y, hnew = orc.state_update("fp32", "weyl", codes, None, p["x"], p["dt"], p["A"],
+                                       p["B"], p["C"], p["D"])
+    # independent float64 evaluation with explicit head -> group broadcasting
+    hpg = nheads // ngroups
+    Bh = np.repeat(p["B"].astype(np.float64), hpg, axis=1)      # [b, h, n]
+    Ch = np.repeat(p["C"].astype(np.float64), hpg, axis=1)
+    dt = p["dt"].astype(np.float64)
+    if family == "mamba1":
+        dA = np.exp(dt[:, :, None, None] * p["A"].astype(np.float64)[None, :, None, :])
+    else:
+        dA = np.exp(dt * p["A"].astype(np.float64)[None, :])[:, :, None, None]
+    w = dt[:, :, None, None] * p["x"].astype(np.float64)[..., None] * Bh[:, :, None, :]
+    h = dA * h0 + w
+    yr = np.einsum("bhpn,bhn->bhp", h, Ch) + p["D"].astype(np.float64)[None, :, None] * p["x"]
+    # a few fp32 roundings of the two terms (no cancellation allowance beyond that)
+    assert np.all(np.abs(hnew - h) <= 2.5e-7 * (np.abs(dA * h0) + np.abs(w)))
+    assert np.array_equal(new.view(np.float32), hnew)
+    scale = np.einsum("bhpn,bhn->bhp", np.abs(h), np.abs(Ch)) + np.abs(p["D"][None, :, None] * p["x"])
+    assert np.all(np.abs(y - yr) <= 1e-6 * scale)
+
+
+def _prop1_run(orc, fmt, rule, f_num, T, h0_code, s, M):
+    """a = 1 (A = 0), constant write w_n = f_n s per column n, T steps from a grid value."""
+    n = len(f_num)
+    w = np.array([Fraction(k, M) * s for k in f_num], dtype=object)
+    wf = np.array([float(v) for v in w], np.float32)
+    assert all(Fraction(float(a)) == b for a, b in zip(wf, w))
+    state = np.full((1, 1, 1, n), h0_code, {"fp16": np.uint16, "bf16": np.uint16}[fmt])
+    one = np.ones((1, 1, 1), np.float32)
+    Us = []
+    for t in range(1, T + 1):
+        state, _, _, _ = orc.state_update(fmt, rule, state, None, one, np.ones((1, 1), np.float32),
+                                          np.zeros((1, n), np.float32), wf[None, None, :],
+                                          np.zeros((1, 1, n), np.float32), None, step=t,
+                                          a_per_state=1, seed=0, layer=0, block=16)
+        Us.append(orc.thresholds(rule, 0, 0, t, 0, n, 16))
+    return state.ravel(), np.array(Us), w
+
+
+@pytest.mark.parametrize("rule", ["rtn", "weyl", "sr"])
+def test_proposition1_error_is_a_count(orc, rule):
+    """e_T = -s (#{t <= T: u_t < 1 - f} - T (1 - f)) exactly, through the fused step."""
+    s = Fraction(1, 1024)                       # fp16 step in [1, 2)
+    M = 1 << 13
+    f_num = [1, 409, 2000, 2458, 3000, 5000, 6143, 8191]  # f = k / 2^13, never exactly 1/2
+    T = 600
+    codes, Us, w = _prop1_run(orc, "fp16", rule, f_num, T, 0x3C00, s, M)
+    got = orc.decode("fp16", codes)
+    for n, k in enumerate(f_num):
+        f = Fraction(k, M)
+        e_T = Fraction(float(got[n])) - (1 + T * w[n])
+        u = np.full(T, 0.5) if rule == "rtn" else Us[:, n] / TWO24
+        count = sum(1 for ut in u if Fraction(ut) < 1 - f)
+        assert e_T == -s * (count - T * (1 - f)), (rule, k)
+        if rule == "rtn":   # Corollary 1(a): linear growth
+            assert e_T == (-s * T * f if f < Fraction(1, 2) else s * T * (1 - f))
+
+
+def test_corollary_b_sr_is_binomial(orc):
+    """Under SR, e_T / s + T f is Binomial(T, f): mean and variance over entries."""
+    T, n, k = 64, 512, 2458
+    M = 1 << 13
+    f = k / M
+    codes, _, w = _prop1_run(orc, "fp16", "sr", [k] * n, T, 0x3C00, Fraction(1, 1024), M)
+    # w < s, so the stored value moves up by whole steps: e_T / s = N_T - T f
+    N_T = np.round((orc.decode("fp16", codes) - 1.0) * 1024).astype(np.int64)
+    mean, var = T * f, T * f * (1 - f)
+    assert abs(N_T.mean() - mean) < 4 * np.sqrt(var / n)
+    assert abs(N_T.var() / var - 1) < 0.25
+
+
+def test_corollary_c_weyl_error_grows_like_log(orc):
+    """sup_f |e_T| = s T D*_T stays below C (1 + log T) for the Weyl thresholds."""
+    i = 987654
+    ratios, sr = [], []
+    U_all = np.array([orc.thresholds("weyl", 0, 0, t, i, 1, 128)[0] for t in range(1, (1 << 14) + 1)])
+    S_all = np.array([orc.thresholds("sr", 0, 0, t, i, 1, 128)[0] for t in range(1, (1 << 14) + 1)])
+    for e in range(4, 15):
+        T = 1 << e
+        ratios.append(T * dsc.star_discrepancy(U_all[:T] / TWO24) / (1 + np.log(T)))
+        sr.append(T * dsc.star_discrepancy(S_all[:T] / TWO24))
+    assert max(ratios) < 1.0
+    assert sr[-1] > 20 * ratios[-1] * (1 + np.log(1 << 14))  # SR grows like sqrt(T)
+
+
+def test_corollary_d_near_rational_increment(orc):
+    """alpha = 1/2 + 2^-12 is as bad as RTN for T <= 2^12 / 8: sup_f |e_T| >= (3/16) s T."""
+    T = 512
+    alpha = 0.5 + 2 ** -12
+    o = 0.3
+    u = np.array([(o + t * alpha) % 1.0 for t in range(1, T + 1)])
+    U = np.floor(u * TWO24).astype(np.uint32)
+    s = 2.0 ** -10
+    worst = 0.0
+    for k in range(1, 1 << 10):
+        f = k / 1024
+        h = 1.0
+        exact = 1.0
+        for t in range(T):
+            exact += f * s
+            h = float(orc.decode("fp16", orc.round_values("fp16", "weyl", [h + f * s], U[t:t + 1]))[0])
+        worst = max(worst, abs(h - exact))
+        if worst >= 3 / 16 * s * T:
+            break
+    assert worst >= 3 / 16 * s * T
+
+
+@pytest.mark.parametrize("fmt", ["fp16", "bf16"])
+def test_lemma_erasure(orc, fmt):
+    """RTN leaves a grid value unchanged when |delta| < s / 2; the dithers do not."""
+    rng = np.random.default_rng(4)
+    n = 256
+    h0 = (1.0 + rng.random(n)).astype(np.float32)
+    codes0 = orc.round_values(fmt, "rtn", h0).astype(np.uint16)
+    hq = orc.decode(fmt, codes0)
+    s = 2.0 ** (-10 if fmt == "fp16" else -7)
+    A = np.full((1, n), -1e-4, np.float32)
+    dt = np.ones((1, 1), np.float32)
+    w = (rng.uniform(-0.3, 0.3, n) * s).astype(np.float32)
+    delta = (np.exp(np.float64(np.float32(-1e-4))) - 1) * hq + w
+    assert np.all(np.abs(delta) < s / 2)
+    state = codes0.reshape(1, 1, 1, n)
+    x = np.ones((1, 1, 1), np.float32)
+    B = w.reshape(1, 1, n)
+    C = np.zeros((1, 1, n), np.float32)
+    new, _, _, _ = orc.state_update(fmt, "rtn", state, None, x, dt, A, B, C, None, step=1)
+    assert np.array_equal(new, state)
+    moved = 0
+    for t in range(1, 9):
+        new, _, _, _ = orc.state_update(fmt, "weyl", state, None, x, dt, A, B, C, None, step=t)
+        moved += np.count_nonzero(new != state)
+    assert moved > 0
+
+
+def test_lemma_noise(orc):
+    """Uniform fractional parts: E r^2 = s^2/12 (RTN) and s^2/6 (SR, Weyl)."""
+    rng = np.random.default_rng(8)
+    n = 200_000
+    x = (1.0 + rng.random(n)).astype(np.float32)
+    s = 2.0 ** -10
+    for rule, want in (("rtn", 1 / 12), ("sr", 1 / 6), ("weyl", 1 / 6)):
+        U = orc.thresholds(rule, 0, 0, 3, 0, n, 16)
+        q = orc.decode("fp16", orc.round_values("fp16", rule, x, U))
+        r2 = np.mean(((q - x.astype(np.float64)) / s) ** 2)
+        assert abs(r2 / want - 1) < 0.02, rule
+
+
+def test_stationary_error_variance(orc):
+    """e_t = a e_(t-1) + r_t with i.i.d. residuals: Var e = sigma_r^2 / (1 - a^2)."""
+    rng = np.random.default_rng(21)
+    n, T, a32 = 2048, 400, np.float32(0.9)
+    s = 2.0 ** -10
+    for rule, sig2 in (("rtn", 1 / 12), ("sr", 1 / 6)):
+        exact = np.full(n, 1.5)
+        codes = orc.round_values("fp16", "rtn", exact.astype(np.float32)).astype(np.uint16)
+        errs = []
+        for t in range(1, T + 1):
+            wv = (np.float32(0.15) + (rng.random(n) * 2 * s).astype(np.float32)).astype(np.float32)
+            hq = orc.decode("fp16", codes)
+            pre = (np.float64(a32) * hq + wv).astype(np.float32)   # exact in fp32 here
+            codes = orc.round_values("fp16", rule, pre, orc.thresholds(rule, 0, 0, t, 0, n, 16)).astype(np.uint16)
+            exact = np.float64(a32) * exact + wv
+            if t > 100:
+                errs.append(orc.decode("fp16", codes) - exact)
+        v = np.var(np.concatenate(errs)) / s ** 2
+        want = sig2 / (1 - float(a32) ** 2)
+        assert abs(v / want - 1) < 0.1, rule
+
+
+def test_decay_bound(orc):
+    """|e_T| <= max_m |sum_{t>=m} r_t| for any rule (Appendix A), in exact arithmetic."""
+    rng = np.random.default_rng(5)
+    for rule in ("rtn", "sr", "weyl"):
+        for entry in range(3):
+            T = 120
+            a = rng.uniform(0.9, 1.0, T).astype(np.float32)
+            w = (rng.standard_normal(T) * 0.01).astype(np.float32)
+            hq = Fraction(1)
+            code = np.array([0x3C00], np.uint16)
+            h = Fraction(1)
+            res = []
+            for t in range(T):
+                pre = np.float32(np.float64(a[t]) * float(hq) + np.float64(w[t]))
+                U = orc.thresholds(rule, 0, 0, t + 1, entry, 1, 16)
+                code = orc.round_values("fp16", rule, [pre], U).astype(np.uint16)
+                new = Fraction(float(orc.decode("fp16", code)[0]))
+                res.append(new - (Fraction(float(a[t])) * hq + Fraction(float(w[t]))))
+                h = Fraction(float(a[t])) * h + Fraction(float(w[t]))
+                hq = new
+            e_T = hq - h
+            tails = [sum(res[m:], Fraction(0)) for m in range(T)]
+            assert abs(e_T) <= max(abs(r) for r in tails)
+
+
+@pytest.mark.parametrize("rule", ["sr", "weyl"])
+def test_dithers_are_unbiased(orc, rule):
+    """E[Q(x)] = x: averaged over steps, the stored value of a fixed x converges to x."""
+    rng = np.random.default_rng(17)
+    x = (1.0 + rng.random(64)).astype(np.float32)
+    T = 4096
+    acc = np.zeros(64)
+    for t in range(T):
+        U = orc.thresholds(rule, 0, 0, t, 0, 64, 16)
+        acc += orc.decode("fp16", orc.round_values("fp16", rule, x, U))
+    bias = (acc / T - x.astype(np.float64)) / 2.0 ** -10
+    tol = 4 * 0.5 / np.sqrt(T) if rule == "sr" else 0.01
+    assert np.all(np.abs(bias) < tol)
+
+
+def test_e4m3_step_uses_group_scale(orc):
+    """E4M3 step: dequantize with the old scale, new scale = max|h_new| / 448."""
+    p = _inputs("mamba2", 2, 4, 8, 32, 2, seed=5)
+    codes, scale = wl.initial_state("e4m3", 2, 4, 8, 32, seed=5)
+    codes, scale = codes.numpy(), scale.numpy()
+    new, sc, y, hnew = orc.state_update("e4m3", "weyl", codes, scale, p["x"], p["dt"], p["A"],
+                                        p["B"], p["C"], p["D"], block=128)
+    m = np.abs(hnew.reshape(8, -1)).max(axis=1).astype(np.float32)
+    assert np.array_equal(sc, (m / np.float32(448.0)).astype(np.float32))
+    deq = orc.dequantize("e4m3", new, sc, 8 * 32).reshape(8, -1)
+    step = np.float32(2.0) ** np.floor(np.log2(np.maximum(np.abs(hnew.reshape(8, -1)) / sc[:, None], 2 ** -6))) / 8 * sc[:, None]
+    assert np.all(np.abs(deq - hnew.reshape(8, -1)) <= step * (1 + 1e-6))

@@ -1,0 +1,169 @@
+"""Pins of the oracle's threshold generators (CPU only).
+
+Expected values come from the paper: the Weyl time sequence 0.618, 0.236,
+0.854 (Section 1), the 32-bit golden increment 2654435769 and Knuth's constant
+2654435761 (Section 5.4), the R2 offset constants and the separation d = 0.0015
+(Appendix B "Offset near-aliasing" and "Dithers"), Observation 2's stream counts
+for a float32 phase, the LD_256 column of Table "Dither sequences" and the
+hash-SR unit-test moments (Appendix B "Decode regime").
+"""
+from decimal import Decimal, getcontext
+
+import numpy as np
+import pytest
+
+from oracle import discrepancy as dsc
+
+TWO24 = 1 << 24
+TWO32 = 1 << 32
+
+
+def test_weyl_constants_from_the_paper(orc):
+    k = orc.weyl_constants()
+    # "the above constants times 2^32", read as rounding to nearest
+    for name, dec in (("A", "0.7548776662"), ("B", "0.5698402910"), ("L", "0.1234567"),
+                      ("S", "0.3141592")):
+        exact = Decimal(dec) * TWO32
+        assert k[name] == int(exact.to_integral_value(rounding="ROUND_HALF_EVEN")), name
+    getcontext().prec = 60
+    alpha = (Decimal(5).sqrt() - 1) / 2          # golden-ratio increment phi - 1
+    assert k["PHI"] == 2654435769 == int((alpha * TWO32).to_integral_value())
+    assert k["PHI"] - 8 == 2654435761            # Knuth's multiplicative-hash constant
+
+
+@pytest.mark.parametrize("entry", [0, 1, 17, 123456789, 2 ** 33 + 5])
+def test_weyl_time_sequence(orc, entry):
+    """Per entry the thresholds advance by alpha = phi - 1: 0.618, 0.236, 0.854 ..."""
+    U = np.array([orc.thresholds("weyl", 3, 7, t, entry, 1, 16)[0] for t in range(4)], np.int64)
+    steps = ((U[1:] - U[0]) % TWO24) / TWO24
+    assert np.allclose(steps, [0.618034, 0.236068, 0.854102], atol=2e-6)
+
+
+def test_weyl_float_form_agrees_for_small_indices(orc):
+    """Hardware form == {o_rc + t alpha} of the float form while r, t are small."""
+    alpha = (5 ** 0.5 - 1) / 2
+    rng = np.random.default_rng(0)
+    for _ in range(300):
+        block = int(rng.choice([16, 128]))
+        i = int(rng.integers(0, 5000))
+        layer, seed, t = int(rng.integers(0, 64)), int(rng.integers(0, 4)), int(rng.integers(0, 5000))
+        r, c = divmod(i, block)
+        o = (0.7548776662 * (r + 1) + 0.5698402910 * (c + 1) + 0.1234567 * layer
+             + 0.3141592 * seed) % 1.0
+        u_float = (o + (t * alpha) % 1.0) % 1.0
+        u_int = orc.thresholds("weyl", seed, layer, t, i, 1, block)[0] / TWO24
+        d = abs(u_int - u_float)
+        assert min(d, 1 - d) < 2e-6
+
+
+def test_r2_offsets_separation(orc):
+    k = orc.weyl_constants()
+    beta, gamma, alpha = k["A"] / TWO32, k["B"] / TWO32, k["PHI"] / TWO32
+    d = dsc.separation(beta, gamma, alpha)
+    assert 0.0014 <= d <= 0.0016                 # the paper: d = 0.0015
+    knuth = 2654435761 / TWO32
+    assert dsc.separation(knuth, knuth, alpha) < 1e-8   # Knuth offsets alias exactly
+
+
+def test_knuth_offsets_alias_with_time(orc):
+    """Observation 1: with o_i = i H the next entry gets this entry's next threshold."""
+    H, PHI = 2654435761, orc.weyl_constants()["PHI"]
+    i = np.arange(0, 4000, dtype=np.uint64)[:, None]
+    t = np.arange(0, 200, dtype=np.uint64)[None, :]
+    knuth = lambda ii, tt: (((ii * H + tt * PHI) % TWO32) >> 8)
+    frac = np.mean(knuth(i + 1, t) == knuth(i, t + 1))
+    assert abs(frac - (1 - 8 / 256)) < 0.005     # coincide except where a carry crosses
+    # the oracle's offsets do not alias
+    U = np.stack([orc.thresholds("weyl", 0, 0, int(tt), 0, 1001, 128) for tt in range(0, 51)])
+    assert np.mean(U[:-1, 1:] == U[1:, :-1]) < 0.01
+
+
+def test_float32_phase_collapses_streams(orc):
+    """Observation 2: a float32 phase leaves at most 2^(p-1-k) streams; the integer one keeps all."""
+    alpha32 = np.float32((5 ** 0.5 - 1) / 2)
+    offsets = (np.arange(1 << 16, dtype=np.float64) / (1 << 16)).astype(np.float32)
+    for t, expect in ((2047, 8192), (8191, 2048), (32767, 512)):
+        phase = np.float32(np.float32(t) * alpha32)
+        s = (offsets + phase).astype(np.float32)
+        frac = (s - np.floor(s)).astype(np.float32)
+        assert len(np.unique(frac)) == expect
+    n = 1 << 14
+    at0 = orc.thresholds("weyl", 0, 0, 0, 0, n, 16)
+    late = orc.thresholds("weyl", 0, 0, 32767, 0, n, 16)
+    assert len(np.unique(late)) == len(np.unique(at0)) >= n - 4
+
+
+def _windows_weyl_oracle(orc, rng, count, W=256):
+    wins = []
+    for _ in range(count):
+        i = int(rng.integers(0, 1 << 30))
+        t0 = int(rng.integers(0, 1 << 20))
+        wins.append(np.array([orc.thresholds("weyl", 0, 0, t0 + t, i, 1, 16)[0]
+                              for t in range(1, W + 1)]) / TWO24)
+    return wins
+
+
+def test_ld256_table(orc):
+    """LD_256 of Table "Dither sequences" (64 random phases; paper values +-12%)."""
+    rng = np.random.default_rng(2026)
+
+    def ld_float(alpha):
+        return dsc.local_discrepancy([dsc.weyl_float(alpha, rng.random(), int(rng.integers(0, 1 << 20)),
+                                                     256) for _ in range(64)])
+
+    phi1 = (5 ** 0.5 - 1) / 2
+    table = {
+        2 ** 0.5 - 1: 0.0069,
+        1 / (2 + (1 + 5 ** 0.5) / 2): 0.0075,
+        phi1: 0.0078,
+        np.e - 2: 0.0097,
+        0.25 + 2 ** -12: 0.1379,
+        1 / 3 + 2 ** -12: 0.2063,
+        0.5 + 2 ** -12: 0.3347,
+    }
+    for alpha, paper in table.items():
+        assert abs(ld_float(alpha) / paper - 1) < 0.12, alpha
+    # the oracle's integer Weyl thresholds of one entry over time
+    ld_int = dsc.local_discrepancy(_windows_weyl_oracle(orc, rng, 64))
+    assert abs(ld_int / 0.0078 - 1) < 0.12
+    # SR: the oracle's hash over 256 steps of random entries (paper: 0.0539)
+    wins = []
+    for _ in range(200):
+        i = int(rng.integers(0, 1 << 30))
+        t0 = int(rng.integers(0, 1 << 20))
+        wins.append(np.array([orc.thresholds("sr", 0, 0, t0 + t, i, 1, 16)[0]
+                              for t in range(1, 257)]) / TWO24)
+    assert abs(dsc.local_discrepancy(wins) / 0.0539 - 1) < 0.08
+
+
+def _moments(u):
+    u = np.asarray(u, np.float64)
+    c = u - u.mean()
+    lag1 = np.dot(c[1:], c[:-1]) / np.dot(c, c)
+    return u.mean(), u.var(), lag1
+
+
+def test_sr_hash_moments(orc):
+    """Hash-SR unit test (paper: mean 0.4997, variance 0.0834, lag-1 -5e-5)."""
+    n = 1 << 20
+    over_entries = orc.thresholds("sr", 0, 0, 5, 0, n, 16) / TWO24
+    m, v, r = _moments(over_entries)
+    se = 1 / np.sqrt(12 * n)
+    assert abs(m - 0.5) < 5 * se and abs(v - 1 / 12) < 5e-4 and abs(r) < 5 / np.sqrt(n)
+    T = 1 << 15
+    over_time = np.array([orc.thresholds("sr", 1, 3, t, 777, 1, 16)[0] for t in range(T)]) / TWO24
+    m, v, r = _moments(over_time)
+    assert abs(m - 0.5) < 5 / np.sqrt(12 * T) and abs(v - 1 / 12) < 2e-3 and abs(r) < 5 / np.sqrt(T)
+
+
+def test_sr_keys_differ_by_seed_layer_step(orc):
+    base = orc.thresholds("sr", 0, 0, 0, 0, 4096, 16)
+    for args in ((1, 0, 0), (0, 1, 0), (0, 0, 1)):
+        other = orc.thresholds("sr", *args, 0, 4096, 16)
+        assert np.mean(base == other) < 0.01
+    # a step's thresholds over entries are a bijection of the entry index (no repeats)
+    assert len(np.unique(orc.thresholds("sr", 0, 0, 9, 0, 1 << 16, 16))) > (1 << 16) - 200
+
+
+def test_rtn_nominal_threshold(orc):
+    assert np.all(orc.thresholds("rtn", 5, 5, 5, 0, 64, 16) == 1 << 23)
