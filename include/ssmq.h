@@ -1,0 +1,172 @@
+/*
+ * ssmq.h -- quantized selective-state update for Mamba-style recurrent state
+ * caches on AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Low-Discrepancy Dither for Quantized Recurrent State Caches".
+ * Each state entry follows h_t = a_t h_(t-1) + w_t (Section 2, eq. (rec)); the
+ * update is computed in fp32 and rounded only when written back (Section 2,
+ * "Low-precision storage") with one of three threshold rules of eq. (dither):
+ * round-to-nearest, stochastic rounding, or the golden-ratio Weyl dither with
+ * per-entry R2 offsets and an integer phase (Appendix B, "Dithers").
+ *
+ * Conventions shared by every entry point:
+ *   - Data pointers are DEVICE pointers (HIP device memory) unless stated. The
+ *     caller owns every buffer and keeps it alive until the work on `stream`
+ *     has completed. Nothing is allocated or retained by the library.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *     Every call only enqueues work and returns; completion is the caller's
+ *     business (e.g. hipStreamSynchronize).
+ *   - All arguments are validated on the host before any HIP call. A rejected
+ *     call returns a non-zero status, touches no memory and leaves a message
+ *     for ssmq_last_error(). A failed kernel launch returns SSMQ_EDEVICE.
+ *   - Tensors are contiguous and row-major, with the layouts given below.
+ *   - Step, layer and seed arithmetic is modulo 2^32.
+ *   - Calls on different streams that write the same memory race; the library
+ *     holds no global mutable state and is otherwise thread-safe.
+ */
+#ifndef SSMQ_H
+#define SSMQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SSMQ_OK = 0,
+    SSMQ_EINVAL = 1,       /* null pointer, bad size or bad enum value          */
+    SSMQ_EUNSUPPORTED = 2, /* valid but not implemented (shape / group layout)  */
+    SSMQ_EALIGN = 3,       /* a pointer misses its required alignment           */
+    SSMQ_EDEVICE = 4       /* the HIP runtime reported an error                 */
+} ssmq_status;
+
+/* Rounding rules, eq. (dither): Q_u(x) = s floor(x/s + u) (Section 2). */
+typedef enum {
+    SSMQ_RTN = 0,  /* round to nearest, ties to even (the native cast)                  */
+    SSMQ_SR = 1,   /* stochastic: u from a counter-based hash of (seed, layer, entry, t) */
+    SSMQ_WEYL = 2  /* Weyl dither: u = top 24 bits of A(r+1)+B(c+1)+L l+S sigma+t Phi    */
+} ssmq_rule;
+
+/* Storage formats (Section 2 "Low-precision storage"; Appendix B "Formats"). */
+typedef enum {
+    SSMQ_FP16 = 0,      /* IEEE binary16 codes, no scale                                 */
+    SSMQ_BF16 = 1,      /* bfloat16 codes, no scale                                      */
+    SSMQ_FP8_E4M3 = 2,  /* OCP E4M3FN codes with one fp32 scale per group, max 448,
+                           saturating                                                    */
+    SSMQ_FP32 = 3       /* unrounded fp32 (a full-precision twin); the rule is ignored   */
+} ssmq_format;
+
+/* Shape of one layer's state cache [batch][nheads][headdim][dstate]. */
+typedef struct {
+    int64_t batch;       /* sequences in the batch (0 is a valid no-op)                   */
+    int32_t nheads;      /* Mamba-2 heads; Mamba-1: d_inner channels                      */
+    int32_t headdim;     /* P rows per head; Mamba-1: 1                                   */
+    int32_t dstate;      /* N, the state dimension                                        */
+    int32_t ngroups;     /* groups sharing B and C; head h uses group h / (nheads/ngroups) */
+    int32_t a_per_state; /* 0: A[nheads] (Mamba-2); 1: A[nheads][dstate] (Mamba-1)        */
+} ssmq_dims;
+
+/* How the state is written back. */
+typedef struct {
+    int32_t rule;          /* ssmq_rule                                                    */
+    int32_t format;        /* ssmq_format                                                  */
+    int32_t dither_block;  /* Weyl offsets: block r = i / dither_block, position
+                              c = i % dither_block of the flat entry index i; a power of
+                              two. 16 for Mamba models, the state dimension for hybrids
+                              (Section 2 "Low-precision storage")                           */
+    int32_t scale_group;   /* E4M3: entries per fp32 scale, a power of two >= 16 that
+                              divides headdim*dstate; 0 = one scale per head               */
+    uint32_t seed;         /* sigma (Appendix B "Dithers"; SR key)                          */
+    uint32_t layer;        /* l (Appendix B "Dithers"; SR key)                              */
+    uint32_t step;         /* t, the integer phase counter (Section 5.4, "Computing the
+                              phase in float32": an integer phase keeps every stream)      */
+    uint32_t reserved;     /* must be 0                                                    */
+    uint64_t entry_base;   /* global flat index of entry 0 of this tensor, a multiple of
+                              16; lets a shard reproduce the unsharded thresholds           */
+} ssmq_qparams;
+
+/*
+ * ssmq_state_update -- one decode step of the selective-state update, in place.
+ *
+ * Defines (Section 2, eq. (rec); Appendix B "Runners", Mamba-1 and Mamba-2):
+ *   h_prev = decode(state)                 (E4M3: code value * old group scale)
+ *   dA     = exp(dt * A)                   (per head, or per (head, n) for Mamba-1)
+ *   h_new  = dA * h_prev + (dt * x_p) * B_n
+ *   y_p    = sum_n C_n * h_new + D * x_p   (from the unrounded h_new)
+ *   state  = Q_u(h_new) under (rule, format); E4M3 first sets each group scale to
+ *            max|h_new| / 448 and rounds h_new * (1/scale) (Appendix B "Formats").
+ * Entry i = entry_base + flat index uses threshold u_(i,step) (see ssmq_dither_fill).
+ *
+ * Arguments (device pointers; alignment in brackets):
+ *   state        [batch][nheads][headdim][dstate] codes (2 B fp16/bf16, 1 B E4M3,
+ *                4 B fp32), read and overwritten [16 B]
+ *   state_scale  E4M3 only: [batch*nheads*headdim*dstate / group] fp32, read (old
+ *                scales) and overwritten (new scales) [4 B]; NULL otherwise
+ *   x            [batch][nheads][headdim] fp32 [4 B]
+ *   dt           [batch][nheads] fp32, the step size after softplus [4 B]
+ *   A            [nheads] [4 B] or [nheads][dstate] [16 B] fp32 (negative decay rates)
+ *   B, C         [batch][ngroups][dstate] fp32 [16 B]
+ *   D            [nheads] fp32, or NULL for no skip term [4 B]
+ *   y            [batch][nheads][headdim] fp32, written [4 B]
+ * Requirements: a state row splits into 16-byte chunks (dstate % 8 == 0 for
+ * fp16/bf16, % 16 for E4M3, % 4 for fp32) whose count is a power of two <= 64;
+ * nheads % ngroups == 0. E4M3 groups are either one head (when headdim*dstate is
+ * 4096, 8192, 16384 or 32768 entries and A is per head) or a power of two of at
+ * most 1024 entries. Other shapes return SSMQ_EUNSUPPORTED.
+ */
+ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void* state,
+                              float* state_scale, const float* x, const float* dt,
+                              const float* A, const float* B, const float* C, const float* D,
+                              float* y, void* stream);
+
+/*
+ * ssmq_requantize -- write fp32 values into a storage format under a rule.
+ *
+ * The rounding step alone (Section 2, eq. (dither); Appendix B "Formats"):
+ * codes[k] = Q_u(h[k]) with the threshold of entry entry_base + k. For E4M3 each
+ * group of consecutive entries (q->scale_group, or head_size when that is 0)
+ * gets scale[g] = fl32(max|h| / 448), flushed to 0 below 2^-126 (then every
+ * code of the group is a signed zero), and codes of fl32(h * fl32(1 / scale))
+ * rounded on the E4M3 grid after saturation to +-448. A result of zero keeps
+ * the sign of its input; NaN gives the canonical NaN code.
+ *
+ * Arguments: n_entries >= 0; head_size > 0 (used only for E4M3 with
+ * scale_group 0); h [n_entries] fp32 [16 B]; codes [n_entries] codes [16 B];
+ * scale E4M3 only [n_entries / group] fp32 (written), else NULL [4 B].
+ * E4M3 groups must be multiples of 16 that divide n_entries; entry_base must be
+ * a multiple of 16.
+ */
+ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t head_size,
+                            const float* h, void* codes, float* scale, void* stream);
+
+/*
+ * ssmq_dither_fill -- the 24-bit thresholds U (u = U / 2^24) of entries
+ * entry_base .. entry_base + n - 1 at one (seed, layer, step).
+ *
+ *   SSMQ_WEYL: top 24 bits of (A(r+1) + B(c+1) + L layer + S seed + t Phi) mod 2^32,
+ *              r = i / dither_block, c = i % dither_block; A, B, L, S are 2^32 times
+ *              0.7548776662, 0.5698402910, 0.1234567, 0.3141592 rounded to nearest and
+ *              Phi = 2654435769 (Appendix B "Dithers"; Section 5.4).
+ *   SSMQ_SR:   top 24 bits of fmix32(i * 0x9E3779B1 + K) with the per-step key
+ *              K = fmix32(fmix32(fmix32(seed) ^ layer * 0xC2B2AE3D) ^ t * 0x85EBCA77)
+ *              (Appendix B "Decode regime", hash SR; fmix32 = MurmurHash3 finalizer).
+ *   SSMQ_RTN:  2^23 (u = 1/2) everywhere; nearest rounding breaks exact ties to even.
+ * Arguments: n >= 0; dither_block a power of two; U24 [n] uint32 output [4 B];
+ * any entry_base.
+ */
+ssmq_status ssmq_dither_fill(int32_t rule, uint32_t seed, uint32_t layer, uint32_t step,
+                             uint64_t entry_base, int64_t n, int32_t dither_block,
+                             uint32_t* U24, void* stream);
+
+/* Static text for a status code. Never NULL. */
+const char* ssmq_status_string(ssmq_status s);
+
+/* Detail of the last non-OK status returned on this host thread ("" if none). */
+const char* ssmq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSMQ_H */

@@ -1,0 +1,230 @@
+// ssmq_abi.cpp -- the C ABI of include/ssmq.h: host-side validation, launch
+// geometry and dispatch. Every check runs before the first HIP call, so a
+// rejected call never touches the device.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "ssmq.h"
+#include "ssmq_device.hpp"
+#include "ssmq_launch.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+ssmq_status fail(ssmq_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+ssmq_status ok() {
+  g_last_error[0] = '\0';
+  return SSMQ_OK;
+}
+
+bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+int log2i(int64_t v) {
+  int r = 0;
+  while ((int64_t{1} << r) < v) ++r;
+  return r;
+}
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int code_bytes(int format) {
+  return format == SSMQ_FP8_E4M3 ? 1 : (format == SSMQ_FP32 ? 4 : 2);
+}
+int chunk_entries(int format) { return 16 / code_bytes(format); }
+
+// Threshold parameters of one call (Appendix B "Dithers"; hash SR).
+ssmq::Thr make_thr(int rule, uint32_t seed, uint32_t layer, uint32_t step, int32_t block) {
+  ssmq::Thr th{};
+  th.lb = static_cast<uint32_t>(log2i(block));
+  if (rule == SSMQ_WEYL) {
+    th.key = ssmq::kWeylA + ssmq::kWeylB + ssmq::kWeylL * layer + ssmq::kWeylS * seed +
+             ssmq::kWeylPhi * step;
+  } else if (rule == SSMQ_SR) {
+    uint32_t k = ssmq::fmix32(seed);
+    k = ssmq::fmix32(k ^ (layer * ssmq::kSrLayer));
+    k = ssmq::fmix32(k ^ (step * ssmq::kSrStep));
+    th.key = k;
+  }
+  return th;
+}
+
+ssmq_status check_qparams(const ssmq_qparams* q) {
+  if (!q) return fail(SSMQ_EINVAL, "qparams is NULL");
+  if (q->rule < SSMQ_RTN || q->rule > SSMQ_WEYL) return fail(SSMQ_EINVAL, "unknown rule %d", q->rule);
+  if (q->format < SSMQ_FP16 || q->format > SSMQ_FP32)
+    return fail(SSMQ_EINVAL, "unknown format %d", q->format);
+  if (q->reserved != 0) return fail(SSMQ_EINVAL, "qparams.reserved must be 0");
+  if (!is_pow2(q->dither_block) || q->dither_block > (1 << 30))
+    return fail(SSMQ_EINVAL, "dither_block %d is not a power of two in [1, 2^30]", q->dither_block);
+  if (q->entry_base % 16 != 0)
+    return fail(SSMQ_EINVAL, "entry_base %llu is not a multiple of 16",
+                static_cast<unsigned long long>(q->entry_base));
+  if (q->scale_group < 0) return fail(SSMQ_EINVAL, "scale_group is negative");
+  return SSMQ_OK;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a == 0 || b == 0) { *out = 0; return true; }
+  if (a > INT64_MAX / b) return false;
+  *out = a * b;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ssmq_status_string(ssmq_status s) {
+  switch (s) {
+    case SSMQ_OK: return "ok";
+    case SSMQ_EINVAL: return "invalid argument";
+    case SSMQ_EUNSUPPORTED: return "unsupported shape or layout";
+    case SSMQ_EALIGN: return "misaligned pointer";
+    case SSMQ_EDEVICE: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* ssmq_last_error(void) { return g_last_error; }
+
+ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void* state,
+                              float* state_scale, const float* x, const float* dt,
+                              const float* A, const float* B, const float* C, const float* D,
+                              float* y, void* stream) {
+  if (!dims) return fail(SSMQ_EINVAL, "dims is NULL");
+  ssmq_status st = check_qparams(q);
+  if (st != SSMQ_OK) return st;
+  const ssmq_dims& d = *dims;
+  if (d.batch < 0) return fail(SSMQ_EINVAL, "batch %lld < 0", static_cast<long long>(d.batch));
+  if (d.nheads < 1 || d.headdim < 1 || d.dstate < 1 || d.ngroups < 1)
+    return fail(SSMQ_EINVAL, "nheads, headdim, dstate and ngroups must be >= 1");
+  if (d.nheads % d.ngroups != 0)
+    return fail(SSMQ_EINVAL, "nheads %d is not a multiple of ngroups %d", d.nheads, d.ngroups);
+  if (d.a_per_state != 0 && d.a_per_state != 1)
+    return fail(SSMQ_EINVAL, "a_per_state must be 0 or 1");
+  if (!state || !x || !dt || !A || !B || !C || !y)
+    return fail(SSMQ_EINVAL, "state, x, dt, A, B, C and y must not be NULL");
+  const bool fp8 = q->format == SSMQ_FP8_E4M3;
+  if (fp8 && !state_scale) return fail(SSMQ_EINVAL, "E4M3 needs state_scale");
+  if (!aligned(state, 16) || !aligned(B, 16) || !aligned(C, 16) || (d.a_per_state && !aligned(A, 16)))
+    return fail(SSMQ_EALIGN, "state, B, C (and A[nheads][dstate]) must be 16-byte aligned");
+  if (!aligned(x, 4) || !aligned(dt, 4) || !aligned(A, 4) || !aligned(y, 4) ||
+      (D && !aligned(D, 4)) || (fp8 && !aligned(state_scale, 4)))
+    return fail(SSMQ_EALIGN, "fp32 arrays must be 4-byte aligned");
+
+  const int V = chunk_entries(q->format);
+  if (d.dstate % V != 0 || !is_pow2(d.dstate / V) || d.dstate / V > 64)
+    return fail(SSMQ_EUNSUPPORTED,
+                "dstate %d: rows must be a power-of-two number (<= 64) of %d-entry chunks",
+                d.dstate, V);
+  int64_t head_size = 0, n_total = 0, bh = 0;
+  if (!mul_ok(d.headdim, d.dstate, &head_size) || !mul_ok(d.batch, d.nheads, &bh) ||
+      !mul_ok(bh, head_size, &n_total))
+    return fail(SSMQ_EINVAL, "state size overflows int64");
+  int64_t group = 0;
+  if (fp8) {
+    group = q->scale_group ? q->scale_group : head_size;
+    if (group % 16 != 0 || group > head_size || head_size % group != 0)
+      return fail(SSMQ_EINVAL, "scale_group %lld must be a multiple of 16 dividing headdim*dstate",
+                  static_cast<long long>(group));
+  }
+  if (n_total == 0) return ok();
+
+  ssmq::UpdateArgs a{};
+  a.state = state; a.scale = state_scale; a.x = x; a.dt = dt; a.A = A; a.B = B; a.C = C;
+  a.D = D; a.y = y;
+  a.batch = d.batch; a.nheads = d.nheads; a.headdim = d.headdim; a.dstate = d.dstate;
+  a.ngroups = d.ngroups; a.heads_per_group = d.nheads / d.ngroups;
+  a.lanes_per_row = d.dstate / V; a.lr_shift = log2i(a.lanes_per_row);
+  a.head_size = head_size; a.n_chunks = n_total / V;
+  a.entry_base = q->entry_base;
+  a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block);
+  a.group = static_cast<int32_t>(group);
+
+  // head-tile kernel when a head fills 256 threads x {1,2,4,8} chunks
+  const int64_t per_pass = 256LL * V;
+  const int64_t cpt = (head_size % per_pass == 0) ? head_size / per_pass : 0;
+  const bool small_groups_ok = !fp8 || (is_pow2(group / 16) && group / 16 <= 64);
+  int kind = -1;
+  if (d.a_per_state == 0 && (cpt == 1 || cpt == 2 || cpt == 4 || cpt == 8) &&
+      (!fp8 || group == head_size || small_groups_ok) && bh <= 0x7FFFFFFFLL) {
+    kind = 0;
+    a.lanes_per_group = fp8 ? (group == head_size ? 0 : static_cast<int32_t>(group / 16)) : 1;
+  } else if (small_groups_ok) {
+    kind = 1;
+    a.lanes_per_group = fp8 ? static_cast<int32_t>(group / 16) : 1;
+    if ((a.n_chunks + 511) / 512 > 0x7FFFFFFFLL)
+      return fail(SSMQ_EUNSUPPORTED, "state too large for one launch");
+  } else {
+    return fail(SSMQ_EUNSUPPORTED,
+                "E4M3 scale group of %lld entries: supported are powers of two up to 1024 "
+                "entries, or one scale per head when a head tile fills a workgroup",
+                static_cast<long long>(group));
+  }
+  hipError_t e = ssmq::launch_update(a, q->format, q->rule, kind, static_cast<int>(cpt),
+                                     d.a_per_state != 0, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t head_size,
+                            const float* h, void* codes, float* scale, void* stream) {
+  ssmq_status st = check_qparams(q);
+  if (st != SSMQ_OK) return st;
+  if (n_entries < 0) return fail(SSMQ_EINVAL, "n_entries < 0");
+  const bool fp8 = q->format == SSMQ_FP8_E4M3;
+  int64_t group = 0;
+  if (fp8) {
+    group = q->scale_group ? q->scale_group : head_size;
+    if (group <= 0 || group % 16 != 0)
+      return fail(SSMQ_EINVAL, "E4M3 group %lld must be a positive multiple of 16",
+                  static_cast<long long>(group));
+    if (n_entries % group != 0)
+      return fail(SSMQ_EINVAL, "n_entries is not a multiple of the E4M3 group");
+  }
+  if (n_entries == 0) return ok();
+  if (!h || !codes || (fp8 && !scale)) return fail(SSMQ_EINVAL, "h, codes (and scale) must not be NULL");
+  if (!aligned(h, 16) || !aligned(codes, 16) || (fp8 && !aligned(scale, 4)))
+    return fail(SSMQ_EALIGN, "h and codes must be 16-byte aligned, scale 4-byte aligned");
+  ssmq::RequantArgs a{};
+  a.h = h; a.codes = codes; a.scale = scale; a.n = n_entries; a.group = group;
+  a.entry_base = q->entry_base;
+  a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block);
+  a.lanes_per_group = 64;
+  if (fp8 && group / 16 <= 64 && is_pow2(group / 16)) a.lanes_per_group = static_cast<int32_t>(group / 16);
+  if (!fp8 && (n_entries + 16 * 256 - 1) / (16 * 256) > 0x7FFFFFFFLL)
+    return fail(SSMQ_EUNSUPPORTED, "too many entries for one launch");
+  hipError_t e = ssmq::launch_requant(a, q->format, q->rule, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+ssmq_status ssmq_dither_fill(int32_t rule, uint32_t seed, uint32_t layer, uint32_t step,
+                             uint64_t entry_base, int64_t n, int32_t dither_block,
+                             uint32_t* U24, void* stream) {
+  if (rule < SSMQ_RTN || rule > SSMQ_WEYL) return fail(SSMQ_EINVAL, "unknown rule %d", rule);
+  if (n < 0) return fail(SSMQ_EINVAL, "n < 0");
+  if (!is_pow2(dither_block) || dither_block > (1 << 30))
+    return fail(SSMQ_EINVAL, "dither_block %d is not a power of two in [1, 2^30]", dither_block);
+  if (n == 0) return ok();
+  if (!U24) return fail(SSMQ_EINVAL, "U24 is NULL");
+  if (!aligned(U24, 4)) return fail(SSMQ_EALIGN, "U24 must be 4-byte aligned");
+  if ((n + 1023) / 1024 > 0x7FFFFFFFLL) return fail(SSMQ_EUNSUPPORTED, "n too large for one launch");
+  ssmq::DitherArgs a{};
+  a.out = U24; a.n = n; a.entry_base = entry_base;
+  a.thr = make_thr(rule, seed, layer, step, dither_block);
+  hipError_t e = ssmq::launch_dither(a, rule, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

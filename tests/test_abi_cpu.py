@@ -1,0 +1,106 @@
+"""The C ABI library on the CPU: it loads, exports what include/ssmq.h declares,
+and rejects bad arguments on the host before any HIP call (no GPU needed;
+only calls that must fail validation, or are empty, are made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ssmq.h")
+
+EINVAL, EUNSUPPORTED, EALIGN = 1, 2, 3
+FAKE = 0x10000  # a 16-byte aligned, never dereferenced address
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_39185_amd import _binding
+    if not os.path.exists(_binding.LIBRARY):
+        pytest.skip("libssmq.so has not been built")
+    return _binding
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\S.*?\b(ssmq_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_exports_every_declared_function(lib):
+    names = declared_functions()
+    assert set(names) == set(lib.EXPORTS)
+    L = lib.library()
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(lib):
+    L = lib.library()
+    assert L.ssmq_status_string(0) == b"ok"
+    assert L.ssmq_status_string(99) == b"unknown status"
+
+
+def _update(lib, dims, q, **ptrs):
+    p = dict(state=FAKE, scale=None, x=FAKE, dt=FAKE, A=FAKE, B=FAKE, C=FAKE, D=None, y=FAKE)
+    p.update(ptrs)
+    L = lib.library()
+    return L.ssmq_state_update(None if dims is None else ctypes.byref(dims),
+                               None if q is None else ctypes.byref(q), p["state"], p["scale"],
+                               p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"], p["y"], None)
+
+
+def test_state_update_validation(lib):
+    D, Q = lib.Dims, lib.qparams
+    good = D(1, 4, 64, 128, 2, 0)
+    L = lib.library()
+    assert _update(lib, None, Q("weyl", "bf16")) == EINVAL
+    assert _update(lib, good, None) == EINVAL
+    q = Q("weyl", "bf16"); q.rule = 7
+    assert _update(lib, good, q) == EINVAL
+    q = Q("weyl", "bf16"); q.format = 9
+    assert _update(lib, good, q) == EINVAL
+    q = Q("weyl", "bf16"); q.reserved = 1
+    assert _update(lib, good, q) == EINVAL
+    assert _update(lib, good, Q("weyl", "bf16", dither_block=24)) == EINVAL
+    assert _update(lib, good, Q("weyl", "bf16", entry_base=8)) == EINVAL
+    assert _update(lib, D(1, 4, 64, 128, 3, 0), Q("weyl", "bf16")) == EINVAL
+    assert b"ngroups" in L.ssmq_last_error()
+    assert _update(lib, D(-1, 4, 64, 128, 2, 0), Q("weyl", "bf16")) == EINVAL
+    assert _update(lib, D(1, 4, 64, 128, 2, 2), Q("weyl", "bf16")) == EINVAL
+    assert _update(lib, good, Q("weyl", "bf16"), x=None) == EINVAL
+    assert _update(lib, good, Q("weyl", "e4m3")) == EINVAL            # no scale
+    assert _update(lib, good, Q("weyl", "bf16"), state=FAKE + 8) == EALIGN
+    assert _update(lib, good, Q("weyl", "bf16"), B=FAKE + 4) == EALIGN
+    assert _update(lib, good, Q("weyl", "bf16"), x=FAKE + 2) == EALIGN
+    assert _update(lib, D(1, 4, 64, 24, 2, 0), Q("weyl", "bf16")) == EUNSUPPORTED
+    assert _update(lib, D(1, 4, 64, 1024, 2, 0), Q("weyl", "bf16")) == EUNSUPPORTED
+    assert _update(lib, good, Q("weyl", "e4m3", scale_group=48), scale=FAKE) == EINVAL
+    assert _update(lib, good, Q("weyl", "e4m3", scale_group=2048), scale=FAKE) == EUNSUPPORTED
+    # an empty batch is a valid no-op that never reaches the device
+    assert _update(lib, D(0, 4, 64, 128, 2, 0), Q("weyl", "bf16")) == 0
+    assert L.ssmq_last_error() == b""
+
+
+def test_requantize_validation(lib):
+    L = lib.library()
+    Q = lib.qparams
+    assert L.ssmq_requantize(None, 16, 0, FAKE, FAKE, None, None) == EINVAL
+    assert L.ssmq_requantize(ctypes.byref(Q("sr", "bf16")), -1, 0, FAKE, FAKE, None, None) == EINVAL
+    assert L.ssmq_requantize(ctypes.byref(Q("sr", "bf16")), 0, 0, None, None, None, None) == 0
+    assert L.ssmq_requantize(ctypes.byref(Q("sr", "bf16")), 16, 0, FAKE + 4, FAKE, None, None) == EALIGN
+    assert L.ssmq_requantize(ctypes.byref(Q("sr", "e4m3")), 32, 0, FAKE, FAKE, FAKE, None) == EINVAL
+    assert L.ssmq_requantize(ctypes.byref(Q("sr", "e4m3", scale_group=16)), 40, 0, FAKE, FAKE,
+                             FAKE, None) == EINVAL
+    assert L.ssmq_requantize(ctypes.byref(Q("sr", "e4m3", scale_group=16)), 32, 0, FAKE, FAKE,
+                             None, None) == EINVAL
+
+
+def test_dither_fill_validation(lib):
+    L = lib.library()
+    assert L.ssmq_dither_fill(5, 0, 0, 0, 0, 16, 16, FAKE, None) == EINVAL
+    assert L.ssmq_dither_fill(2, 0, 0, 0, 0, -1, 16, FAKE, None) == EINVAL
+    assert L.ssmq_dither_fill(2, 0, 0, 0, 0, 16, 3, FAKE, None) == EINVAL
+    assert L.ssmq_dither_fill(2, 0, 0, 0, 0, 16, 16, None, None) == EINVAL
+    assert L.ssmq_dither_fill(2, 0, 0, 0, 0, 16, 16, FAKE + 2, None) == EALIGN
+    assert L.ssmq_dither_fill(2, 0, 0, 0, 0, 0, 16, None, None) == 0

@@ -1,0 +1,346 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bit-exact for thresholds and for requantize (identical fp32 inputs); the fused
+step at the stated bar: y within 1e-5 relative, at most 0.01 % of stored
+entries differing, each by at most one storage ulp.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_39185_amd import workloads as wl
+
+from ._parity import DEV, assert_codes, check_step, say
+
+pytestmark = pytest.mark.gpu
+
+TWO24 = 1 << 24
+
+
+@pytest.fixture(scope="module")
+def ssmq():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_39185_amd as m
+    m.library()
+    return m
+
+
+# --------------------------------------------------------------------------
+# thresholds
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+@pytest.mark.parametrize("block", [1, 16, 128, 1 << 20])
+@pytest.mark.parametrize("entry_base,n", [(0, 0), (0, 1), (3, 1000), (2 ** 33 + 7, 4099),
+                                          (1 << 20, 65536)])
+def test_dither_fill_bit_exact(ssmq, rule, block, entry_base, n):
+    say(f"case dither_fill {rule} block {block} base {entry_base} n {n}")
+    out = torch.full((max(n, 1),), -1, dtype=torch.int32, device=DEV)
+    ssmq.dither_fill(out[:n] if n else out[:0], rule=rule, seed=5, layer=9, step=123456,
+                     entry_base=entry_base, dither_block=block)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint32)[:n]
+    want = oracle.thresholds(rule, 5, 9, 123456, entry_base, n, block)
+    assert np.array_equal(got, want)
+    if n == 0:
+        assert out.cpu().numpy()[0] == -1
+
+
+# --------------------------------------------------------------------------
+# requantize: bit-exact on identical fp32 inputs, edge suites included
+# --------------------------------------------------------------------------
+def _edge_values(fmt, rng, n_random, entry_base, rule, block, seed, layer, step):
+    """Random values over many binades plus values on and next to rounding points."""
+    e = rng.integers(-40 if fmt != "bf16" else -135, 17 if fmt != "bf16" else 128, n_random)
+    m = rng.integers(0, 1 << 23, n_random).astype(np.uint64)
+    s = rng.integers(0, 2, n_random).astype(np.uint64)
+    bits = (s << 31) | (np.clip(e + 127, 1, 254).astype(np.uint64) << 23) | m
+    x = bits.astype(np.uint32).view(np.float32)
+    specials = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, -np.nan, 1.0, -1.0, 65504.0, 65519.0,
+                         65520.0, -65520.0, 448.0, 464.0, 3.3895314e38, 3.4028235e38, 1e-45,
+                         -1e-45, 5.9604645e-08, -2.9802322e-08, 1.0 + 2 ** -11, 1.0 + 2 ** -8,
+                         2 ** -14, -2 ** -14, 2 ** -15 + 2 ** -25, 1e-38, -1e-40],
+                        dtype=np.float32)
+    x = np.concatenate([x, specials])
+    # values exactly at / next to the dither's rounding point of their own entry
+    U = oracle.thresholds(rule, seed, layer, step, entry_base, x.size, block)
+    lo = oracle.decode(fmt, oracle.round_values(fmt, "weyl", x, np.zeros_like(U)))
+    hi = oracle.decode(fmt, oracle.round_values(fmt, "weyl", x, np.full_like(U, TWO24 - 1)))
+    ok = np.isfinite(lo) & np.isfinite(hi) & (hi != lo) & (rng.random(x.size) < 0.3)
+    pt = hi - (U / TWO24) * (hi - lo)
+    p32 = pt.astype(np.float32)
+    sel = np.nonzero(ok)[0]
+    jitter = rng.integers(-1, 2, sel.size)
+    x = x.copy()
+    x[sel] = np.where(jitter < 0, np.nextafter(p32[sel], np.float32(-np.inf)),
+                      np.where(jitter > 0, np.nextafter(p32[sel], np.float32(np.inf)), p32[sel]))
+    return x.astype(np.float32)
+
+
+@pytest.mark.parametrize("fmt", ["fp16", "bf16", "fp32"])
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+@pytest.mark.parametrize("n,entry_base,block", [(16 * 4096, 0, 16), (100_003, 48, 128),
+                                                (15, 16, 1), (0, 0, 16)])
+def test_requantize_bit_exact(ssmq, fmt, rule, n, entry_base, block):
+    say(f"case requantize {fmt} {rule} n {n} base {entry_base} block {block}")
+    rng = np.random.default_rng(n + block)
+    x = _edge_values(fmt, rng, max(n - 27, 0), entry_base, rule, block, 3, 4, 77)[:n]
+    h = torch.from_numpy(x).to(DEV)
+    dt = {"fp16": torch.int16, "bf16": torch.int16, "fp32": torch.int32}[fmt]
+    codes = torch.zeros(n, dtype=dt, device=DEV)
+    ssmq.requantize(h, codes, None, rule=rule, fmt=fmt, dither_block=block, seed=3, layer=4,
+                    step=77, entry_base=entry_base)
+    torch.cuda.synchronize()
+    got = wl.to_numpy_codes(fmt, codes)
+    want, _ = oracle.requantize(fmt, rule, x, seed=3, layer=4, step=77, entry_base=entry_base,
+                                block=block)
+    if fmt == "fp32":
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+    else:
+        assert np.array_equal(got, want), np.nonzero(got != want)[0][:10]
+
+
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+@pytest.mark.parametrize("group,n_groups", [(16, 700), (128, 300), (8192, 9), (48, 33),
+                                            (2048, 5)])
+def test_requantize_e4m3_bit_exact(ssmq, rule, group, n_groups):
+    say(f"case requantize e4m3 {rule} group {group} x {n_groups}")
+    rng = np.random.default_rng(group)
+    n = group * n_groups
+    mag = np.exp(rng.uniform(-30, 10, n_groups)).astype(np.float32)
+    x = (rng.standard_normal(n).astype(np.float32) * np.repeat(mag, group)).astype(np.float32)
+    x[:group] = 0.0                                       # zero group
+    x[group:2 * group] *= np.float32(1e-38)              # group whose scale is subnormal
+    x[2 * group + 3] = np.nan                             # NaN inside a live group
+    # tiny entries next to large ones: E4M3 subnormal outputs
+    x[3 * group:4 * group] = (rng.standard_normal(group) * 1e-7).astype(np.float32)
+    x[3 * group] = 100.0
+    h = torch.from_numpy(x).to(DEV)
+    codes = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    scale = torch.full((n_groups,), -1.0, dtype=torch.float32, device=DEV)
+    ssmq.requantize(h, codes, scale, rule=rule, fmt="e4m3", scale_group=group, seed=1, layer=2,
+                    step=3, entry_base=32, dither_block=128)
+    torch.cuda.synchronize()
+    want, wscale = oracle.requantize("e4m3", rule, x, seed=1, layer=2, step=3, entry_base=32,
+                                     block=128, group=group)
+    assert np.array_equal(scale.cpu().numpy(), wscale)
+    got = codes.cpu().numpy()
+    assert np.array_equal(got, want), np.nonzero(got != want)[0][:10]
+
+
+# --------------------------------------------------------------------------
+# fused step
+# --------------------------------------------------------------------------
+M2_SMALL = ("mamba2", 2, 4, 64, 128, 2)
+
+
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+@pytest.mark.parametrize("fmt,q", [("bf16", {"dither_block": 128}), ("fp16", {"dither_block": 16}),
+                                   ("fp32", {}), ("e4m3", {"dither_block": 128}),
+                                   ("e4m3", {"scale_group": 16}), ("e4m3", {"scale_group": 128}),
+                                   ("e4m3", {"scale_group": 1024, "dither_block": 1})])
+def test_step_head_tile(ssmq, rule, fmt, q):
+    check_step(fmt, rule, *M2_SMALL, seed=10, what="head tile", step=5, layer=2, **q)
+
+
+SHAPES = [
+    # (family, batch, nheads, headdim, dstate, ngroups)
+    ("mamba1", 3, 200, 1, 16, 1),       # Mamba-1 rows, ragged grid tail
+    ("mamba1", 1, 1536, 1, 16, 1),      # the small Mamba-1 workload
+    ("mamba2", 3, 6, 64, 64, 3),        # head of 4096 entries
+    ("mamba2", 2, 4, 32, 128, 1),       # head tile of 4096 entries
+    ("mamba2", 2, 2, 64, 256, 2),       # long rows (32 / 16 lanes)
+    ("mamba2", 5, 3, 8, 16, 1),         # small heads -> row kernel
+    ("mamba2", 1, 2, 1, 128, 1),        # one row per head
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("fmt", ["fp16", "bf16", "e4m3", "fp32"])
+def test_step_shapes(ssmq, shape, fmt):
+    family, batch, nheads, headdim, dstate, ngroups = shape
+    head = headdim * dstate
+    q = {"dither_block": 16, "step": 9, "layer": 1}
+    if fmt == "e4m3" and head > 1024 and not (family == "mamba2" and head % 4096 == 0):
+        q["scale_group"] = 64
+    for rule in ("rtn", "sr", "weyl"):
+        check_step(fmt, rule, family, batch, nheads, headdim, dstate, ngroups, seed=20,
+                   what=f"shape {shape}", **q)
+
+
+def test_step_no_skip_term_and_entry_base(ssmq):
+    """D = NULL and a nonzero entry_base (a shard of a larger tensor)."""
+    A, _ = wl.layer_params("mamba2", 4, 128, 3)
+    x, dt, B, C = wl.step_inputs(2, 4, 64, 128, 2, 4)
+    codes, _ = wl.initial_state("bf16", 2, 4, 64, 128, 5)
+    from ._parity import run_update, oracle_update
+    q = dict(dither_block=128, entry_base=3 * 8192 * 4, step=11)
+    g = run_update("bf16", "weyl", codes, None, x, dt, A, B, C, None, **q)
+    r = oracle_update("bf16", "weyl", codes, None, x, dt, A, B, C, None, **q)
+    assert_codes("bf16", g[0], r[0], "entry_base")
+
+
+def test_sharding_reproduces_unsharded(ssmq):
+    """Two batch halves with entry_base offsets give the unsharded result bit for bit."""
+    from ._parity import run_update
+    b, H, P, N, G = 4, 4, 64, 128, 2
+    A, D = wl.layer_params("mamba2", H, N, 6)
+    x, dt, B, C = wl.step_inputs(b, H, P, N, G, 7)
+    for fmt in ("bf16", "e4m3"):
+        codes, scale = wl.initial_state(fmt, b, H, P, N, 8)
+        full = run_update(fmt, "weyl", codes, scale, x, dt, A, B, C, D, dither_block=128, step=3)
+        half = b // 2
+        parts = []
+        for k in range(2):
+            sl = slice(k * half, (k + 1) * half)
+            sc = None if scale is None else scale[k * half * H:(k + 1) * half * H].contiguous()
+            parts.append(run_update(fmt, "weyl", codes[sl].contiguous(), sc, x[sl].contiguous(),
+                                    dt[sl].contiguous(), A, B[sl].contiguous(),
+                                    C[sl].contiguous(), D, dither_block=128, step=3,
+                                    entry_base=k * half * H * P * N))
+        assert np.array_equal(np.concatenate([p[0] for p in parts]), full[0])
+        assert np.array_equal(np.concatenate([p[2] for p in parts]), full[2])
+
+
+def test_deterministic(ssmq):
+    from ._parity import run_update
+    A, D = wl.layer_params("mamba2", 8, 128, 1)
+    x, dt, B, C = wl.step_inputs(4, 8, 64, 128, 2, 2)
+    codes, scale = wl.initial_state("e4m3", 4, 8, 64, 128, 3)
+    a = run_update("e4m3", "sr", codes, scale, x, dt, A, B, C, D, step=4)
+    b = run_update("e4m3", "sr", codes, scale, x, dt, A, B, C, D, step=4)
+    assert all(np.array_equal(u, v) for u, v in zip(a, b))
+
+
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+def test_small_mamba1_workload_64_steps(ssmq, rule):
+    """Mamba-1, batch 1, d_inner 1536, d_state 16, fp16: 64 teacher-forced steps."""
+    import paper_2609_39185_amd as m
+    w = wl.WORKLOADS["m1_small"]
+    A, D = wl.layer_params("mamba1", w.nheads, w.dstate, 100)
+    codes, _ = wl.initial_state("fp16", w.batch, w.nheads, 1, w.dstate, 101)
+    st = codes.to(DEV)
+    Ad, Dd = A.to(DEV), D.to(DEV)
+    worst = 0
+    for t in range(1, w.steps + 1):
+        x, dt, B, C = wl.step_inputs(w.batch, w.nheads, 1, w.dstate, 1, 1000 + t)
+        before = wl.to_numpy_codes("fp16", st)
+        y = torch.empty(x.shape, dtype=torch.float32, device=DEV)
+        m.state_update(st, None, x.to(DEV), dt.to(DEV), Ad, B.to(DEV), C.to(DEV), Dd, y,
+                       rule=rule, fmt="fp16", dither_block=16, step=t)
+        torch.cuda.synchronize()
+        r_codes, _, r_y, _ = oracle.state_update("fp16", rule, before, None, x.numpy(),
+                                                 dt.numpy(), A.numpy(), B.numpy(), C.numpy(),
+                                                 D.numpy(), step=t, block=16)
+        got = wl.to_numpy_codes("fp16", st)
+        nd = int(np.count_nonzero(got != r_codes))
+        worst = max(worst, nd)
+        assert nd <= 1e-4 * got.size
+    say(f"  m1_small {rule}: worst step had {worst} differing stored entries")
+
+
+def test_proposition1_through_the_kernel(ssmq):
+    """a = 1, constant write: e_T = -s(#{u_t < 1-f} - T(1-f)) on the GPU state."""
+    import paper_2609_39185_amd as m
+    n, T = 64, 300
+    f_num = np.arange(1, n + 1) * 127
+    s = 2.0 ** -10
+    w = (f_num / 8192 * s).astype(np.float32)
+    st = torch.full((1, 1, 1, n), 0x3C00, dtype=torch.int16, device=DEV)
+    one = torch.ones((1, 1, 1), device=DEV)
+    A = torch.zeros((1, n), device=DEV)
+    B = torch.from_numpy(w).reshape(1, 1, n).to(DEV)
+    C = torch.zeros((1, 1, n), device=DEV)
+    y = torch.empty((1, 1, 1), device=DEV)
+    thr = torch.empty(n, dtype=torch.int32, device=DEV)
+    count = np.zeros(n, np.int64)
+    for t in range(1, T + 1):
+        m.state_update(st, None, one, torch.ones((1, 1), device=DEV), A, B, C, None, y,
+                       rule="weyl", fmt="fp16", step=t)
+        m.dither_fill(thr, rule="weyl", step=t)
+        torch.cuda.synchronize()
+        u = thr.cpu().numpy().view(np.uint32) / TWO24
+        count += u < 1 - f_num / 8192
+    h = oracle.decode("fp16", wl.to_numpy_codes("fp16", st).ravel())
+    e_T = h - (1.0 + T * w.astype(np.float64))
+    assert np.allclose(e_T, -s * (count - T * (1 - f_num / 8192)), rtol=0, atol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# full-size workloads, sampled tiles against the oracle
+# --------------------------------------------------------------------------
+def _full_size_sampled(ssmq, name, fmt, rule, n_tiles=24):
+    import paper_2609_39185_amd as m
+    w = wl.WORKLOADS[name]
+    b, H, P, N, G = w.batch, w.nheads, w.headdim, w.dstate, w.ngroups
+    say(f"case full size {name} {fmt} {rule}: {w.entries_per_layer} entries")
+    A, D = wl.layer_params(w.family, H, N, 500, device=DEV)
+    x, dt, B, C = wl.step_inputs(b, H, P, N, G, 501, device=DEV)
+    codes, scale = wl.initial_state(fmt, b, H, P, N, 502, device=DEV)
+    before = codes.clone()
+    sbefore = None if scale is None else scale.clone()
+    y = torch.empty((b, H, P), dtype=torch.float32, device=DEV)
+    m.state_update(codes, scale, x, dt, A, B, C, D, y, rule=rule, fmt=fmt,
+                   dither_block=w.dither_block, step=777, layer=5)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    tiles = rng.choice(b * H, size=n_tiles, replace=False)
+    tiles[0], tiles[-1] = 0, b * H - 1
+    hpg = H // G
+    for tile in tiles:
+        bb, hh = divmod(int(tile), H)
+        gg = hh // hpg
+        cs = lambda t: t.detach().cpu()
+        r_codes, r_scale, r_y, r_h = oracle.state_update(
+            fmt, rule, wl.to_numpy_codes(fmt, cs(before[bb:bb + 1, hh:hh + 1])),
+            None if sbefore is None else cs(sbefore[tile:tile + 1]).numpy(),
+            cs(x[bb:bb + 1, hh:hh + 1]).numpy(), cs(dt[bb:bb + 1, hh:hh + 1]).numpy(),
+            cs(A[hh:hh + 1]).numpy(), cs(B[bb:bb + 1, gg:gg + 1]).numpy(),
+            cs(C[bb:bb + 1, gg:gg + 1]).numpy(), cs(D[hh:hh + 1]).numpy(),
+            step=777, layer=5, block=w.dither_block, entry_base=int(tile) * P * N)
+        got = wl.to_numpy_codes(fmt, cs(codes[bb:bb + 1, hh:hh + 1]))
+        from ._parity import code_stats
+        nd, ulp = code_stats(fmt, got, r_codes)
+        assert nd <= 1 and ulp <= 1, (tile, nd, ulp)
+        if scale is not None:
+            assert np.array_equal(cs(scale[tile:tile + 1]).numpy(), r_scale)
+        Ch = cs(C[bb, gg]).numpy().astype(np.float64)
+        mag = np.abs(Ch[None, :] * r_h[0, 0]).sum(-1) + abs(float(D[hh]) * cs(x[bb, hh]).numpy())
+        yg = cs(y[bb, hh]).numpy().astype(np.float64)
+        assert np.all(np.abs(yg - r_y[0, 0]) <= 1e-5 * (mag + np.abs(r_y[0, 0])))
+
+
+@pytest.mark.parametrize("fmt,rule", [("bf16", "weyl"), ("bf16", "sr"), ("e4m3", "weyl"),
+                                      ("e4m3", "rtn")])
+def test_full_size_hybrid_stack_layer(ssmq, fmt, rule):
+    _full_size_sampled(ssmq, "hybrid_m2_stack", fmt, rule)
+
+
+def test_full_size_fp8_decode(ssmq):
+    _full_size_sampled(ssmq, "m2_b64_fp8", "e4m3", "sr")
+
+
+def test_full_size_ssd_decode(ssmq):
+    _full_size_sampled(ssmq, "m2_ssd_b8", "bf16", "weyl")
+
+
+# --------------------------------------------------------------------------
+# errors surface as exceptions, before any work is queued
+# --------------------------------------------------------------------------
+def test_errors(ssmq):
+    import paper_2609_39185_amd as m
+    st = torch.zeros((1, 4, 64, 128), dtype=torch.int16, device=DEV)
+    x = torch.zeros((1, 4, 64), device=DEV)
+    dt = torch.zeros((1, 4), device=DEV)
+    A = torch.zeros(4, device=DEV)
+    B = torch.zeros((1, 3, 128), device=DEV)
+    y = torch.zeros((1, 4, 64), device=DEV)
+    with pytest.raises(m.SsmqError) as e:
+        m.state_update(st, None, x, dt, A, B, B, None, y, rule="weyl", fmt="bf16")
+    assert e.value.status == 1
+    with pytest.raises(m.SsmqError) as e:
+        m.state_update(st, None, x, dt, A, B[:, :2], B[:, :2], None, y, rule="weyl", fmt="bf16",
+                       dither_block=24)
+    assert e.value.status == 1
+    with pytest.raises(ValueError):
+        m.state_update(st.cpu(), None, x, dt, A, B, B, None, y, rule="weyl", fmt="bf16")
