@@ -41,10 +41,18 @@ int code_bytes(int format) {
 }
 int chunk_entries(int format) { return 16 / code_bytes(format); }
 
-// Threshold parameters of one call (Appendix B "Dithers"; hash SR).
-ssmq::Thr make_thr(int rule, uint32_t seed, uint32_t layer, uint32_t step, int32_t block) {
+// Threshold parameters of one call (Appendix B "Dithers"; hash SR) and the
+// offset of entry k within a chunk whose first flat index is a multiple of 16.
+ssmq::Thr make_thr(int rule, uint32_t seed, uint32_t layer, uint32_t step, int32_t block,
+                   uint32_t toff[16]) {
   ssmq::Thr th{};
   th.lb = static_cast<uint32_t>(log2i(block));
+  const uint32_t mask = static_cast<uint32_t>(block) - 1u;
+  for (uint32_t k = 0; k < 16; ++k) {
+    if (rule == SSMQ_WEYL) toff[k] = ssmq::kWeylA * (k >> th.lb) + ssmq::kWeylB * (k & mask);
+    else if (rule == SSMQ_SR) toff[k] = k * ssmq::kSrEntry;
+    else toff[k] = 0u;
+  }
   if (rule == SSMQ_WEYL) {
     th.key = ssmq::kWeylA + ssmq::kWeylB + ssmq::kWeylL * layer + ssmq::kWeylS * seed +
              ssmq::kWeylPhi * step;
@@ -145,33 +153,65 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
   a.batch = d.batch; a.nheads = d.nheads; a.headdim = d.headdim; a.dstate = d.dstate;
   a.ngroups = d.ngroups; a.heads_per_group = d.nheads / d.ngroups;
   a.lanes_per_row = d.dstate / V; a.lr_shift = log2i(a.lanes_per_row);
+  a.dstate_shift = log2i(d.dstate);
   a.head_size = head_size; a.n_chunks = n_total / V;
   a.entry_base = q->entry_base;
-  a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block);
-  a.group = static_cast<int32_t>(group);
-
-  // head-tile kernel when a head fills 256 threads x {1,2,4,8} chunks
-  const int64_t per_pass = 256LL * V;
-  const int64_t cpt = (head_size % per_pass == 0) ? head_size / per_pass : 0;
+  a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block, a.toff);
+  a.group_shift = fp8 && is_pow2(group) ? log2i(group) : 0;
   const bool small_groups_ok = !fp8 || (is_pow2(group / 16) && group / 16 <= 64);
-  int kind = -1;
-  if (d.a_per_state == 0 && (cpt == 1 || cpt == 2 || cpt == 4 || cpt == 8) &&
-      (!fp8 || group == head_size || small_groups_ok) && bh <= 0x7FFFFFFFLL) {
-    kind = 0;
-    a.lanes_per_group = fp8 ? (group == head_size ? 0 : static_cast<int32_t>(group / 16)) : 1;
-  } else if (small_groups_ok) {
-    kind = 1;
-    a.lanes_per_group = fp8 ? static_cast<int32_t>(group / 16) : 1;
-    if ((a.n_chunks + 511) / 512 > 0x7FFFFFFFLL)
-      return fail(SSMQ_EUNSUPPORTED, "state too large for one launch");
-  } else {
-    return fail(SSMQ_EUNSUPPORTED,
-                "E4M3 scale group of %lld entries: supported are powers of two up to 1024 "
-                "entries, or one scale per head when a head tile fills a workgroup",
-                static_cast<long long>(group));
+
+  // Slab kernels for per-head A: a workgroup owns whole rows of one head, two
+  // 16-byte chunks per thread; with one E4M3 scale per head the workgroup owns
+  // the whole head.
+  int cfg = -1;
+  const int64_t head_chunks = head_size / V;
+  if (d.a_per_state == 0 && fp8 && group == head_size) {
+    switch (head_chunks) {
+      case 256: cfg = ssmq::kSlab256x1; break;
+      case 512: cfg = ssmq::kSlab256x2; break;
+      case 1024: cfg = ssmq::kSlab256x4; break;
+      case 2048: cfg = ssmq::kSlab512x4; break;
+      case 4096: cfg = ssmq::kSlab1024x4; break;
+      case 8192: cfg = ssmq::kSlab1024x8; break;
+      default: break;
+    }
+    if (cfg >= 0) { a.slabs_per_head = 1; a.lanes_per_group = 0; }
   }
-  hipError_t e = ssmq::launch_update(a, q->format, q->rule, kind, static_cast<int>(cpt),
-                                     d.a_per_state != 0, static_cast<hipStream_t>(stream));
+  if (cfg < 0 && d.a_per_state == 0 && small_groups_ok && head_chunks % 256 == 0) {
+    cfg = (head_chunks % 512 == 0) ? ssmq::kSlab256x2 : ssmq::kSlab256x1;
+    a.slabs_per_head = static_cast<int32_t>(
+        head_chunks / (ssmq::kSlabThreads[cfg] * ssmq::kSlabChunks[cfg]));
+    a.lanes_per_group = fp8 ? static_cast<int32_t>(group / 16) : 1;
+  }
+  if (cfg >= 0) {  // threshold base advance per pass of NT chunks
+    const int64_t step_entries = static_cast<int64_t>(ssmq::kSlabThreads[cfg]) * V;
+    a.pass_thr_ok = 1;
+    if (q->rule == SSMQ_WEYL) {
+      a.pass_thr_ok = (step_entries % q->dither_block) == 0;
+      a.pass_thr_inc = ssmq::kWeylA * static_cast<uint32_t>(step_entries >> a.thr.lb);
+    } else if (q->rule == SSMQ_SR) {
+      a.pass_thr_inc = static_cast<uint32_t>(step_entries) * ssmq::kSrEntry;
+    }
+  }
+  if (cfg >= 0 && bh * a.slabs_per_head > 0x7FFFFFFFLL)
+    return fail(SSMQ_EUNSUPPORTED, "state too large for one launch");
+  a.div_nheads = ssmq::make_fastdiv(static_cast<uint32_t>(d.nheads));
+  a.div_hpg = ssmq::make_fastdiv(static_cast<uint32_t>(a.heads_per_group));
+  if (cfg >= 0) a.div_slabs = ssmq::make_fastdiv(static_cast<uint32_t>(a.slabs_per_head));
+  if (cfg < 0) {
+    if (!small_groups_ok)
+      return fail(SSMQ_EUNSUPPORTED,
+                  "E4M3 scale group of %lld entries: supported are powers of two up to 1024 "
+                  "entries, or one scale per head of 4096 to 131072 entries with A per head",
+                  static_cast<long long>(group));
+    if ((n_total >> a.dstate_shift) > 0xFFFFFFFFLL || (a.n_chunks + 255) / 256 > 0x7FFFFFFFLL)
+      return fail(SSMQ_EUNSUPPORTED, "state too large for one launch");
+    cfg = ssmq::kRowKernel;
+    a.lanes_per_group = fp8 ? static_cast<int32_t>(group / 16) : 1;
+    a.div_headdim = ssmq::make_fastdiv(static_cast<uint32_t>(d.headdim));
+  }
+  hipError_t e = ssmq::launch_update(a, q->format, q->rule, cfg, d.a_per_state != 0,
+                                     static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
   return ok();
 }
@@ -198,7 +238,7 @@ ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t he
   ssmq::RequantArgs a{};
   a.h = h; a.codes = codes; a.scale = scale; a.n = n_entries; a.group = group;
   a.entry_base = q->entry_base;
-  a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block);
+  a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block, a.toff);
   a.lanes_per_group = 64;
   if (fp8 && group / 16 <= 64 && is_pow2(group / 16)) a.lanes_per_group = static_cast<int32_t>(group / 16);
   if (!fp8 && (n_entries + 16 * 256 - 1) / (16 * 256) > 0x7FFFFFFFLL)
@@ -221,7 +261,8 @@ ssmq_status ssmq_dither_fill(int32_t rule, uint32_t seed, uint32_t layer, uint32
   if ((n + 1023) / 1024 > 0x7FFFFFFFLL) return fail(SSMQ_EUNSUPPORTED, "n too large for one launch");
   ssmq::DitherArgs a{};
   a.out = U24; a.n = n; a.entry_base = entry_base;
-  a.thr = make_thr(rule, seed, layer, step, dither_block);
+  uint32_t unused[16];
+  a.thr = make_thr(rule, seed, layer, step, dither_block, unused);
   hipError_t e = ssmq::launch_dither(a, rule, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
   return ok();

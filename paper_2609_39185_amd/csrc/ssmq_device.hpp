@@ -1,20 +1,32 @@
 // ssmq_device.hpp -- device primitives of the quantized state update (gfx950).
 //
-// Formats, thresholds and the dithered rounding of eq. (dither) (Section 2),
-// written on bit patterns for the GPU. The rounding of a finite fp32 value x
-// into a format whose grid drops k of x's fraction bits is decided in integer
-// arithmetic:
-//   eq. (dither) rounds the magnitude up exactly when u >= 1 - f (x > 0) or
-//   u < f' (x < 0, f' the magnitude's fraction). With U = 2^24 u and R the k
-//   dropped bits, for k <= 24 both cases read "R + (U_e >> (24 - k)) >= 2^k",
-//   where U_e = U for x >= 0 and 2^24 - 1 - U for x < 0. Adding U_e >> (24-k)
-//   to the magnitude and truncating therefore performs the rounding, carry into
-//   the exponent included. In the 32-bit threshold word thr (U = thr >> 8),
-//   U_e >> (24 - k) = (thr ^ signmask) >> (32 - k).
-// The normal ranges of fp16 (k = 13), bf16 (k = 16) and E4M3 (k = 20) satisfy
-// k <= 24. Below the smallest normal of fp16 and E4M3 the grid step is fixed,
-// x / step has an exact fp32 integer part and fraction F, and the rule becomes
-// the exact fp32 comparison F >= 1 - u (x >= 0) or F > u (x < 0).
+// Formats, thresholds and the dithered rounding of eq. (dither) (Section 2).
+//
+// The rule. Write |x| = s (K + F) on the local grid of the format (K integer,
+// F in [0, 1)), u = U / 2^24 with U the 24-bit threshold. Eq. (dither) is a
+// signed floor, s floor(x/s + u): a positive x rounds up iff u >= 1 - F, a
+// negative x rounds away from zero iff u < F. With R the k dropped fraction
+// bits, for k <= 24 both read "R + (U_e >> (24 - k)) >= 2^k" where U_e = U for
+// x >= 0 and U_e = 2^24 - 1 - U for x < 0, i.e. the magnitude is rounded up
+// iff adding U_e's top k bits to it carries. In a 32-bit threshold word thr
+// (U = thr >> 8), U_e is the top 24 bits of thr ^ signmask(x).
+//
+// Fast paths (the gfx950 conversions, checked on the device against the exact
+// rule): v_cvt_sr_{bf16,f16,fp8}_f32(x, r) round |x| up iff the top 24 bits of
+// r, added as above, carry; fed r = thr ^ signmask they implement eq. (dither)
+// wherever k <= 24. The plain casts and v_cvt_pk_fp8_f32 are round-to-nearest-
+// even. What they do not cover goes to the exact software path below, inside a
+// branch that is taken by a wave only when one of its lanes needs it:
+//   bf16  nothing (k = 16 everywhere; NaN and Inf come out canonical);
+//   fp16  the subnormal range |x| < 2^-14 (the conversion is not exact there);
+//   E4M3  NaN (the conversion loses its sign) and |q| < 2^-10, where k > 24.
+// E4M3 values are first clamped to +-448 (saturation); the conversions do not
+// saturate above 464.
+//
+// Exact software path. Normal ranges use the carry rule on the magnitude bits.
+// Below the smallest normal of fp16 and E4M3 the grid step is fixed, |x| / step
+// has an exact fp32 integer part I and fraction F, and the rule is the exact
+// fp32 comparison F >= 1 - u (x >= 0) or F > u (x < 0).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -56,39 +68,44 @@ template <> struct Traits<kBF16> { static constexpr int bytes = 2, V = 8; };
 template <> struct Traits<kE4M3> { static constexpr int bytes = 1, V = 16; };
 template <> struct Traits<kFP32> { static constexpr int bytes = 4, V = 4; };
 
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+typedef _Float16 v2h __attribute__((ext_vector_type(2)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
 // ---------------------------------------------------------------------------
 // Thresholds. A chunk is V consecutive entries starting at a flat index e0 that
-// is a multiple of V; entry k of the chunk has index e0 + k.
+// is a multiple of V; entry k of the chunk uses thr_word(base(e0), off[k]) with
+// off[k] precomputed on the host (Weyl: A (k >> lb) + B (k & (block-1)); SR:
+// k * 0x9E3779B1).
 // ---------------------------------------------------------------------------
-// Weyl accumulator of entry e0 (without the (r+1), (c+1) ones, folded in key).
-__device__ inline uint32_t weyl_base(uint64_t e0, const Thr& th) {
-  const uint32_t r = static_cast<uint32_t>(e0 >> th.lb);
-  const uint32_t c = static_cast<uint32_t>(e0) & ((1u << th.lb) - 1u);
-  return kWeylA * r + kWeylB * c + th.key;
-}
-// Increment from entry e0 to e0 + k of an aligned chunk (valid when e0 is a
-// multiple of the chunk size and the block is a power of two).
-__device__ inline uint32_t weyl_off(uint32_t k, const Thr& th) {
-  return kWeylA * (k >> th.lb) + kWeylB * (k & ((1u << th.lb) - 1u));
-}
-
 template <int R>
 __device__ inline uint32_t thr_base(uint64_t e0, const Thr& th) {
-  if constexpr (R == kWEYL) return weyl_base(e0, th);
-  else if constexpr (R == kSR) return static_cast<uint32_t>(e0) * kSrEntry + th.key;
-  else return 0u;
+  if constexpr (R == kWEYL) {
+    const uint32_t r = static_cast<uint32_t>(e0 >> th.lb);
+    const uint32_t c = static_cast<uint32_t>(e0) & ((1u << th.lb) - 1u);
+    return kWeylA * r + kWeylB * c + th.key;
+  } else if constexpr (R == kSR) {
+    return static_cast<uint32_t>(e0) * kSrEntry + th.key;
+  } else {
+    return 0u;
+  }
 }
 template <int R>
-__device__ inline uint32_t thr_word(uint32_t base, uint32_t k, const Thr& th) {
-  if constexpr (R == kWEYL) return base + weyl_off(k, th);
-  else if constexpr (R == kSR) return fmix32(base + k * kSrEntry);
+__device__ inline uint32_t thr_word(uint32_t base, uint32_t off) {
+  if constexpr (R == kWEYL) return base + off;
+  else if constexpr (R == kSR) return fmix32(base + off);
   else return 0x80000000u;
 }
 
+// thr ^ signmask(x) in the top 24 bits (the low byte is don't-care).
+__device__ inline uint32_t signed_thr(uint32_t thr, float x) {
+  return thr ^ static_cast<uint32_t>(static_cast<int32_t>(__float_as_uint(x)) >> 24);
+}
+
 // ---------------------------------------------------------------------------
-// Rounding fp32 -> code. thr: 32-bit threshold word, U = thr >> 8.
+// Exact software rounding fp32 -> code.
 // ---------------------------------------------------------------------------
-// Fixed-step region: |x| = T * step with T < 2^10 exact in fp32.
 template <bool RTN>
 __device__ inline uint32_t round_fixed_step(float T, uint32_t neg, uint32_t thr) {
   const float I = floorf(T);
@@ -174,49 +191,211 @@ __device__ inline uint32_t round_code(float x, uint32_t thr) {
 }
 
 // ---------------------------------------------------------------------------
-// Decoding code -> fp32 (exact). E4M3 goes through the fp16 grid: the E4M3
-// value of code c equals 256 times the binary16 value of
-// ((c & 0x7F) << 7) | ((c & 0x80) << 8), subnormals included, so
-// fl32(v * s) = fl32(fp16value * (256 s)) when 256 s is exact.
+// Chunk quantizers: V fp32 values (E4M3: already multiplied by 1/scale) -> one
+// 16-byte chunk of codes, fast path plus the exact path for rare entries.
 // ---------------------------------------------------------------------------
-__device__ inline float fp16_bits_to_float(uint32_t h) {
-  _Float16 v = __builtin_bit_cast(_Float16, static_cast<uint16_t>(h));
-  return static_cast<float>(v);
-}
 template <int F>
-__device__ inline float decode_code(uint32_t c, float s256) {
-  if constexpr (F == kBF16) return __uint_as_float(c << 16);
-  else if constexpr (F == kFP16) return fp16_bits_to_float(c);
-  else if constexpr (F == kE4M3) {
-    const float v = fp16_bits_to_float(((c & 0x7Fu) << 7) | ((c & 0x80u) << 8)) * s256;
-    return ((c & 0x7Fu) == 0x7Fu) ? __uint_as_float(0x7FC00000u) : v;
-  } else return __uint_as_float(c);
+__device__ inline void patch_code(uint32_t (&w)[4], int k, uint32_t c) {
+  if constexpr (Traits<F>::bytes == 4) {
+    w[k] = c;
+  } else {
+    constexpr int bits = Traits<F>::bytes * 8;
+    constexpr int per = 32 / bits;
+    const int i = k / per, sh = (k % per) * bits;
+    const uint32_t mask = ((1u << bits) - 1u) << sh;
+    w[i] = (w[i] & ~mask) | ((c << sh) & mask);
+  }
 }
 
-// Unpack / pack the codes of one 16-byte chunk.
-template <int F>
-__device__ inline uint32_t chunk_code(const uint4& raw, int k) {
-  const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-  if constexpr (Traits<F>::bytes == 4) return w[k];
-  else if constexpr (Traits<F>::bytes == 2) return (w[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu;
-  else return (w[k >> 2] >> ((k & 3) * 8)) & 0xFFu;
+template <int F, int R>
+__device__ inline bool needs_exact_path(float v) {
+  if constexpr (F == kE4M3) {
+    if constexpr (R == kRTN) return v != v;                            // NaN
+    else return !(__builtin_fabsf(v) >= 0x1p-10f);                     // NaN or k > 24
+  } else if constexpr (F == kFP16) {
+    if constexpr (R == kRTN) return false;
+    else return __builtin_fabsf(v) < 0x1p-14f;                         // subnormal range
+  } else {
+    return false;
+  }
 }
-template <int F>
-__device__ inline uint4 pack_chunk(const uint32_t (&c)[Traits<F>::V]) {
-  uint32_t w[4];
+
+// Does any value of the chunk need the exact path? maybe_nan comes from the
+// caller (a NaN anywhere in the chunk, possibly a false alarm); the magnitude
+// tests use the chunk minimum (fminf ignores NaN).
+template <int F, int R, int V>
+__device__ inline bool chunk_is_rare(const float (&v)[V], bool maybe_nan) {
+  if constexpr (F == kBF16 || F == kFP32) return false;
+  else if constexpr (F == kFP16 && R == kRTN) return false;
+  else if constexpr (F == kE4M3 && R == kRTN) return maybe_nan;
+  else {
+    float mn = __builtin_fabsf(v[0]);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if constexpr (Traits<F>::bytes == 4) w[i] = c[i];
-    else if constexpr (Traits<F>::bytes == 2) w[i] = c[2 * i] | (c[2 * i + 1] << 16);
-    else w[i] = c[4 * i] | (c[4 * i + 1] << 8) | (c[4 * i + 2] << 16) | (c[4 * i + 3] << 24);
+    for (int k = 1; k < V; ++k) mn = fminf(mn, __builtin_fabsf(v[k]));
+    if constexpr (F == kFP16) return mn < 0x1p-14f;
+    else return maybe_nan || !(mn >= 0x1p-10f);
+  }
+}
+
+// Whether any of the chunk's values is NaN, for callers without a cheaper test.
+template <int V>
+__device__ inline bool chunk_has_nan(const float (&v)[V]) {
+  bool n = false;
+#pragma unroll
+  for (int k = 0; k < V; k += 2) n |= __builtin_isunordered(v[k], v[k + 1]);
+  return n;
+}
+
+template <int F, int R>
+__device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t base,
+                                       const uint32_t* off, bool maybe_nan) {
+  constexpr int V = Traits<F>::V;
+  uint32_t w[4];
+  if constexpr (F == kFP32) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(v[i]);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  if constexpr (F == kBF16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v2bf p;
+      if constexpr (R == kRTN) {
+        p = (v2bf){static_cast<__bf16>(v[2 * i]), static_cast<__bf16>(v[2 * i + 1])};
+      } else {
+        p = __builtin_amdgcn_cvt_sr_bf16_f32((v2bf){0, 0}, v[2 * i],
+                                             signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]),
+                                             false);
+        p = __builtin_amdgcn_cvt_sr_bf16_f32(
+            p, v[2 * i + 1], signed_thr(thr_word<R>(base, off[2 * i + 1]), v[2 * i + 1]), true);
+      }
+      w[i] = __builtin_bit_cast(uint32_t, p);
+    }
+  } else if constexpr (F == kFP16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v2h p;
+      if constexpr (R == kRTN) {
+        p = (v2h){static_cast<_Float16>(v[2 * i]), static_cast<_Float16>(v[2 * i + 1])};
+      } else {
+        p = __builtin_amdgcn_cvt_sr_f16_f32((v2h){0, 0}, v[2 * i],
+                                            signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]),
+                                            false);
+        p = __builtin_amdgcn_cvt_sr_f16_f32(
+            p, v[2 * i + 1], signed_thr(thr_word<R>(base, off[2 * i + 1]), v[2 * i + 1]), true);
+      }
+      w[i] = __builtin_bit_cast(uint32_t, p);
+    }
+  } else {  // E4M3, values already scaled; clamp = saturation at 448
+    float q[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) q[k] = __builtin_amdgcn_fmed3f(v[k], -448.0f, 448.0f);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int d = 0;
+      if constexpr (R == kRTN) {
+        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[4 * i], q[4 * i + 1], d, false);
+        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[4 * i + 2], q[4 * i + 3], d, true);
+      } else {
+        const int k = 4 * i;
+        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k], signed_thr(thr_word<R>(base, off[k]), q[k]), d, 0);
+        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 1], signed_thr(thr_word<R>(base, off[k + 1]), q[k + 1]), d, 1);
+        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 2], signed_thr(thr_word<R>(base, off[k + 2]), q[k + 2]), d, 2);
+        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 3], signed_thr(thr_word<R>(base, off[k + 3]), q[k + 3]), d, 3);
+      }
+      w[i] = static_cast<uint32_t>(d);
+    }
+  }
+  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, V>(v, maybe_nan)) != 0) {
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      if (needs_exact_path<F, R>(v[k])) patch_code<F>(w, k, round_code<F, R>(v[k], thr_word<R>(base, off[k])));
+    }
   }
   return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// ---------------------------------------------------------------------------
+// Decoding code -> fp32 (exact; E4M3 through v_cvt_pk_f32_fp8, which decodes
+// OCP E4M3 exactly) and the group-scale product for E4M3.
+// ---------------------------------------------------------------------------
+template <int F>
+__device__ inline void decode_chunk(const uint4& raw, float s, float (&out)[Traits<F>::V]) {
+  const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (F == kBF16) {
+      out[2 * i] = __uint_as_float(w[i] << 16);
+      out[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    } else if constexpr (F == kFP16) {
+      const v2h p = __builtin_bit_cast(v2h, w[i]);
+      out[2 * i] = static_cast<float>(p.x);
+      out[2 * i + 1] = static_cast<float>(p.y);
+    } else if constexpr (F == kE4M3) {
+      const v2f lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), false);
+      const v2f hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), true);
+      out[4 * i] = lo.x * s;
+      out[4 * i + 1] = lo.y * s;
+      out[4 * i + 2] = hi.x * s;
+      out[4 * i + 3] = hi.y * s;
+    } else {
+      out[i] = __uint_as_float(w[i]);
+    }
+  }
 }
 
 // E4M3 group scale: s = fl32(m / 448), flushed to zero below 2^-126.
 __device__ inline float e4m3_scale(float m) {
   const float s = m / 448.0f;
   return (s >= 1.17549435e-38f) ? s : 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// Cross-lane reductions over aligned groups of `width` lanes (a power of two
+// <= 64): DPP within 16-lane rows, then swizzles across rows.
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                               CTRL, 0xF, 0xF, false));
+}
+constexpr int kQuadXor1 = 0xB1;     // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;     // quad_perm [2,3,0,1]
+constexpr int kHalfMirror = 0x141;  // lane i <-> 7 - i within 8
+constexpr int kRowMirror = 0x140;   // lane i <-> 15 - i within 16
+
+__device__ inline float lane_sum(float v, int width) {
+  if (width >= 2) v += dpp_f<kQuadXor1>(v);
+  if (width >= 4) v += dpp_f<kQuadXor2>(v);
+  if (width >= 8) v += dpp_f<kHalfMirror>(v);
+  if (width >= 16) v += dpp_f<kRowMirror>(v);
+  if (width >= 32) v += __shfl_xor(v, 16, 64);
+  if (width >= 64) v += __shfl_xor(v, 32, 64);
+  return v;
+}
+template <int CTRL>
+__device__ inline uint32_t dpp_u(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), CTRL, 0xF, 0xF, false));
+}
+// Maximum of unsigned words (bit patterns of non-negative, non-NaN floats).
+__device__ inline uint32_t lane_umax(uint32_t v, int width) {
+  if (width >= 2) v = max(v, dpp_u<kQuadXor1>(v));
+  if (width >= 4) v = max(v, dpp_u<kQuadXor2>(v));
+  if (width >= 8) v = max(v, dpp_u<kHalfMirror>(v));
+  if (width >= 16) v = max(v, dpp_u<kRowMirror>(v));
+  if (width >= 32) v = max(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 16, 64)));
+  if (width >= 64) v = max(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 32, 64)));
+  return v;
+}
+
+// Streaming (nontemporal) 16-byte accesses for the state.
+__device__ inline uint4 load_stream(const void* p) {
+  const v4u v = __builtin_nontemporal_load(static_cast<const v4u*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ inline void store_stream(void* p, const uint4& v) {
+  const v4u w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, static_cast<v4u*>(p));
 }
 
 }  // namespace ssmq

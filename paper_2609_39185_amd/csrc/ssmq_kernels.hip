@@ -1,44 +1,27 @@
 // ssmq_kernels.hip -- HIP kernels of the quantized selective-state update (gfx950).
 //
 // Kernels:
-//   k_update_head  one 256-thread workgroup per (batch, head) tile of a Mamba-2
-//                  state (scalar A per head): dequantize -> exp(dt A) -> FMA
-//                  recurrence -> y = C h + D x -> (E4M3 group scale) -> threshold
-//                  -> round -> store, all in registers; the state crosses HBM
-//                  once each way (Section 2 eq. (rec) and eq. (dither);
-//                  Appendix B "Runners", "Formats", "Dithers").
+//   k_update_slab  Mamba-2 heads (scalar A per head): a workgroup updates a slab
+//                  of rows of one (batch, head) tile: dequantize -> exp(dt A) ->
+//                  FMA recurrence -> y = C h + D x -> (E4M3 group scale) ->
+//                  threshold -> round -> store, in registers, so the state
+//                  crosses HBM once each way (Section 2 eq. (rec) and eq.
+//                  (dither); Appendix B "Runners", "Formats", "Dithers").
 //   k_update_rows  the same step for any row layout (Mamba-1 with A per (channel,
-//                  n), and Mamba-2 shapes that do not fill a head tile).
-//   k_requant      fp32 -> codes for fp16 / bf16 / fp32, 16 entries per thread.
-//   k_requant_e4m3 fp32 -> E4M3 codes with group scales, a wave per group.
+//                  n), and Mamba-2 heads smaller than a slab).
+//   k_requant      fp32 -> codes for fp16 / bf16 / fp32, one chunk per thread.
+//   k_requant_e4m3 fp32 -> E4M3 codes with group scales.
 //   k_dither_fill  the 24-bit thresholds themselves.
 //
-// Thread layout of the update kernels: a chunk is 16 bytes of codes (V entries
-// of one state row). The LR = dstate / V chunks of a row sit in LR consecutive
-// lanes of one wave, so C.h is a reduction over LR lanes and a row's B and C
-// slice is fixed per lane.
+// Layout. A chunk is 16 bytes of codes: V = 8 (fp16, bf16), 16 (E4M3) or 4
+// (fp32) consecutive entries of one state row. The LR = dstate / V chunks of a
+// row sit in LR consecutive lanes of one wave, so a lane's slice of B and C is
+// fixed and C.h is an LR-lane reduction. Each thread owns CPT chunks (one row
+// per pass); the state moves with nontemporal 16-byte accesses, which on this
+// chip stream an in-place read-modify-write fastest with one chunk per thread.
 #include "ssmq_device.hpp"
 
 namespace ssmq {
-
-__device__ inline float lane_sum(float v, int width) {
-  for (int o = width >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-__device__ inline float lane_max(float v, int width) {
-  for (int o = width >> 1; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-
-template <int F>
-__device__ inline uint4 load_chunk(const void* base, int64_t entry) {
-  return *reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(base) +
-                                         entry * Traits<F>::bytes);
-}
-template <int F>
-__device__ inline void store_chunk(void* base, int64_t entry, uint4 v) {
-  *reinterpret_cast<uint4*>(static_cast<uint8_t*>(base) + entry * Traits<F>::bytes) = v;
-}
 
 template <int V>
 __device__ inline void load_floats(const float* p, float (&out)[V]) {
@@ -49,234 +32,246 @@ __device__ inline void load_floats(const float* p, float (&out)[V]) {
   }
 }
 
-// Quantize the V fp32 values of one chunk (E4M3: times r = 1/scale first).
-template <int F, int R>
-__device__ inline uint4 quantize_chunk(const float (&h)[Traits<F>::V], float r, uint64_t e0,
-                                       const Thr& th) {
-  constexpr int V = Traits<F>::V;
-  uint32_t c[V];
-  const uint32_t base = thr_base<R>(e0, th);
-#pragma unroll
-  for (int k = 0; k < V; ++k) {
-    const float v = (F == kE4M3) ? h[k] * r : h[k];
-    c[k] = round_code<F, R>(v, thr_word<R>(base, static_cast<uint32_t>(k), th));
-  }
-  return pack_chunk<F>(c);
+__device__ inline float decay(float dtv, float a) {
+  return static_cast<float>(exp(static_cast<double>(dtv * a)));  // correctly rounded fl32(exp)
 }
 
 // ---------------------------------------------------------------------------
-// Mamba-2 head tile: headdim * dstate = 256 * CPT * V entries per workgroup.
+// Mamba-2 head slabs: NT threads x CPT chunks = a run of whole rows of one head.
 // ---------------------------------------------------------------------------
-template <int F, int R, int CPT>
-__global__ __launch_bounds__(256) void k_update_head(UpdateArgs a) {
+template <int F, int R, int NT, int CPT>
+__global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
   constexpr int V = Traits<F>::V;
+  constexpr int NW = NT / 64;
   const int t = threadIdx.x;
-  const int64_t tile = blockIdx.x;  // b * nheads + h
-  const int hh = static_cast<int>(tile % a.nheads);
-  const int64_t b = tile / a.nheads;
-  const int g = hh / a.heads_per_group;
+  const uint32_t blk = blockIdx.x;
+  const uint32_t tile32 = a.div_slabs.div(blk);  // b * nheads + h
+  const uint32_t slab = blk - tile32 * static_cast<uint32_t>(a.slabs_per_head);
+  const uint32_t b32 = a.div_nheads.div(tile32);
+  const int hh = static_cast<int>(tile32 - b32 * static_cast<uint32_t>(a.nheads));
+  const int g = static_cast<int>(a.div_hpg.div(static_cast<uint32_t>(hh)));
+  const int64_t tile = tile32, b = b32;
   const int cc = t & (a.lanes_per_row - 1);
   const int n0 = cc * V;
-  const int r0 = t >> a.lr_shift;
-  const int rows_per_pass = 256 >> a.lr_shift;
+  const int rows_per_pass = NT >> a.lr_shift;
+  const int r0 = (t >> a.lr_shift) + static_cast<int>(slab) * rows_per_pass * CPT;
   const int64_t tile_base = tile * a.head_size;
+  const int64_t e0 = tile_base + static_cast<int64_t>(r0) * a.dstate + n0;  // first chunk
+  const int64_t pass = static_cast<int64_t>(rows_per_pass) * a.dstate;       // entries per pass
+  uint8_t* const state = static_cast<uint8_t*>(a.state);
 
   uint4 raw[CPT];
   float xv[CPT];
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    const int p = j * rows_per_pass + r0;
-    raw[j] = load_chunk<F>(a.state, tile_base + static_cast<int64_t>(p) * a.dstate + n0);
-    xv[j] = a.x[tile * a.headdim + p];
+    raw[j] = load_stream(state + (e0 + j * pass) * Traits<F>::bytes);
+    xv[j] = a.x[tile * a.headdim + r0 + j * rows_per_pass];
   }
-  float Bv[V], Cv[V];
-  load_floats<V>(a.B + (b * a.ngroups + g) * a.dstate + n0, Bv);
-  load_floats<V>(a.C + (b * a.ngroups + g) * a.dstate + n0, Cv);
   const float dtv = a.dt[tile];
-  const float dA = static_cast<float>(exp(static_cast<double>(dtv * a.A[hh])));
   const float Dv = a.D ? a.D[hh] : 0.0f;
 
-  // old E4M3 scales (times 256, see decode_code)
-  float s256[CPT];
+  // Per-head values are staged once per workgroup in LDS while the state loads
+  // are in flight: B and C of the head's group (one float4 per thread), and
+  // exp(dt A), evaluated by the first wave in double with one final rounding.
+  __shared__ float4 sBC[kMaxDstate / 2];
+  __shared__ float sh[2];
+  const int nq = a.dstate >> 2;  // float4 per vector
+  const float* Bg = a.B + (b * a.ngroups + g) * a.dstate;
+  const float* Cg = a.C + (b * a.ngroups + g) * a.dstate;
+  for (int i = t; i < 2 * nq; i += NT)
+    sBC[i] = (i < nq) ? reinterpret_cast<const float4*>(Bg)[i]
+                      : reinterpret_cast<const float4*>(Cg)[i - nq];
+  if (t < 64) {
+    const float d = decay(dtv, a.A[hh]);
+    if (t == 0) sh[0] = d;
+  }
+  __syncthreads();
+  const float dA = sh[0];
+  float Bv[V], Cv[V];
 #pragma unroll
-  for (int j = 0; j < CPT; ++j) {
-    s256[j] = 0.0f;
-    if constexpr (F == kE4M3) {
-      const int p = j * rows_per_pass + r0;
-      const int64_t e = tile_base + static_cast<int64_t>(p) * a.dstate + n0;
-      s256[j] = a.scale[e / a.group] * 256.0f;
-    }
+  for (int i = 0; i < V / 4; ++i) {
+    const float4 bq = sBC[(n0 >> 2) + i];
+    const float4 cq = sBC[nq + (n0 >> 2) + i];
+    Bv[4 * i] = bq.x; Bv[4 * i + 1] = bq.y; Bv[4 * i + 2] = bq.z; Bv[4 * i + 3] = bq.w;
+    Cv[4 * i] = cq.x; Cv[4 * i + 1] = cq.y; Cv[4 * i + 2] = cq.z; Cv[4 * i + 3] = cq.w;
   }
 
   float h[CPT][V];
+  bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
+    float s_old = 1.0f;
+    if constexpr (F == kE4M3)
+      s_old = (a.lanes_per_group == 0) ? a.scale[tile] : a.scale[(e0 + j * pass) >> a.group_shift];
+    float hp[V];
+    decode_chunk<F>(raw[j], s_old, hp);
     const float dx = dtv * xv[j];
     float ys = 0.0f;
 #pragma unroll
     for (int k = 0; k < V; ++k) {
-      const float hp = decode_code<F>(chunk_code<F>(raw[j], k), s256[j]);
       const float w = dx * Bv[k];
-      h[j][k] = fmaf(dA, hp, w);
+      h[j][k] = fmaf(dA, hp[k], w);
       ys = fmaf(Cv[k], h[j][k], ys);
     }
+    bad[j] = !__builtin_isfinite(ys);
     ys = lane_sum(ys, a.lanes_per_row);
-    if (cc == 0) {
-      const int p = j * rows_per_pass + r0;
-      a.y[tile * a.headdim + p] = ys + Dv * xv[j];
-    }
+    if (cc == 0) a.y[tile * a.headdim + r0 + j * rows_per_pass] = ys + Dv * xv[j];
   }
 
-  // E4M3 scales: per group of a.group entries (lanes_per_group lanes of one
-  // pass), or one per tile (lanes_per_group == 0).
-  float rr[CPT];
+  float r[CPT];
 #pragma unroll
-  for (int j = 0; j < CPT; ++j) rr[j] = 1.0f;
+  for (int j = 0; j < CPT; ++j) r[j] = 1.0f;
   if constexpr (F == kE4M3) {
-    float m[CPT];
+    // Lane maxima of |h| ignore NaN and are >= 0, so the cross-lane maximum can
+    // compare bit patterns as unsigned integers.
+    uint32_t m[CPT];
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
-      m[j] = 0.0f;
+      float mj = 0.0f;
 #pragma unroll
-      for (int k = 0; k < V; ++k) m[j] = fmaxf(m[j], fabsf(h[j][k]));
+      for (int k = 0; k < V; ++k) mj = fmaxf(mj, __builtin_fabsf(h[j][k]));
+      m[j] = __float_as_uint(mj);
     }
-    if (a.lanes_per_group == 0) {
-      __shared__ float red[4];
-      float mm = m[0];
+    if (a.lanes_per_group == 0) {  // one scale for the whole head, which is this workgroup
+      __shared__ uint32_t red[NW];
+      uint32_t mm = m[0];
 #pragma unroll
-      for (int j = 1; j < CPT; ++j) mm = fmaxf(mm, m[j]);
-      mm = lane_max(mm, 64);
+      for (int j = 1; j < CPT; ++j) mm = max(mm, m[j]);
+      mm = lane_umax(mm, 64);
       if ((t & 63) == 0) red[t >> 6] = mm;
       __syncthreads();
-      mm = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-      const float s = e4m3_scale(mm);
-      const float r = (s == 0.0f) ? 0.0f : 1.0f / s;
+      if (t < 64) {  // the first wave turns the maximum into the scale and its reciprocal
+        uint32_t w = red[0];
 #pragma unroll
-      for (int j = 0; j < CPT; ++j) rr[j] = r;
-      if (t == 0) a.scale[tile] = s;
-    } else {
+        for (int i = 1; i < NW; ++i) w = max(w, red[i]);
+        const float s = e4m3_scale(__uint_as_float(w));
+        if (t == 0) {
+          sh[0] = s;
+          sh[1] = (s == 0.0f) ? 0.0f : 1.0f / s;
+          a.scale[tile] = s;
+        }
+      }
+      __syncthreads();
+      const float rs = sh[1];
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) r[j] = rs;
+    } else {  // groups of lanes_per_group consecutive lanes of one pass
 #pragma unroll
       for (int j = 0; j < CPT; ++j) {
-        const float mm = lane_max(m[j], a.lanes_per_group);
-        const float s = e4m3_scale(mm);
-        rr[j] = (s == 0.0f) ? 0.0f : 1.0f / s;
-        const int p = j * rows_per_pass + r0;
-        const int64_t e = tile_base + static_cast<int64_t>(p) * a.dstate + n0;
-        if ((t & (a.lanes_per_group - 1)) == 0) a.scale[e / a.group] = s;
+        const float s = e4m3_scale(__uint_as_float(lane_umax(m[j], a.lanes_per_group)));
+        r[j] = (s == 0.0f) ? 0.0f : 1.0f / s;
+        if ((t & (a.lanes_per_group - 1)) == 0) a.scale[(e0 + j * pass) >> a.group_shift] = s;
       }
     }
   }
 
+  const uint32_t base0 = thr_base<R>(a.entry_base + static_cast<uint64_t>(e0), a.thr);
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    const int p = j * rows_per_pass + r0;
-    const int64_t e = tile_base + static_cast<int64_t>(p) * a.dstate + n0;
-    const uint4 out = quantize_chunk<F, R>(h[j], rr[j], a.entry_base + static_cast<uint64_t>(e),
-                                           a.thr);
-    store_chunk<F>(a.state, e, out);
+    const int64_t e = e0 + j * pass;
+    float v[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) v[k] = (F == kE4M3) ? h[j][k] * r[j] : h[j][k];
+    const uint32_t base = (j == 0) ? base0
+                          : (a.pass_thr_ok ? base0 + static_cast<uint32_t>(j) * a.pass_thr_inc
+                                           : thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr));
+    const uint4 out = quantize_chunk<F, R>(v, base, a.toff, bad[j]);
+    store_stream(state + e * Traits<F>::bytes, out);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Row kernel: any layout whose rows are LR = dstate / V chunks. Each thread
-// handles CPT_ROWS chunks, q = (blockIdx * CPT_ROWS + j) * 256 + t.
+// Row kernel: any layout whose rows are LR = dstate / V chunks; one chunk per
+// thread, chunk q = blockIdx * 256 + t.
 // ---------------------------------------------------------------------------
-constexpr int CPT_ROWS = 2;
-
 template <int F, int R, bool A_PER_STATE>
 __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   constexpr int V = Traits<F>::V;
   const int t = threadIdx.x;
   const int cc = t & (a.lanes_per_row - 1);
   const int n0 = cc * V;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + t;
+  const bool live = q < a.n_chunks;  // whole rows (and groups) are live or dead together
+  const int64_t e = (live ? q : 0) * V;
+  const uint32_t row = static_cast<uint32_t>(e >> a.dstate_shift);  // rows < 2^32 (checked on host)
+  const uint32_t bh = a.div_headdim.div(row);                        // b * nheads + h
+  const uint32_t b = a.div_nheads.div(bh);
+  const int hh = static_cast<int>(bh - b * static_cast<uint32_t>(a.nheads));
+  const int g = static_cast<int>(a.div_hpg.div(static_cast<uint32_t>(hh)));
+  uint8_t* const state = static_cast<uint8_t*>(a.state);
+  const uint4 raw = load_stream(state + e * Traits<F>::bytes);
+  const float xv = a.x[row];
+  const float dtv = a.dt[bh];
+  const float Dv = a.D ? a.D[hh] : 0.0f;
+  float Bv[V], Cv[V], dA[V];
+  load_floats<V>(a.B + (static_cast<int64_t>(b) * a.ngroups + g) * a.dstate + n0, Bv);
+  load_floats<V>(a.C + (static_cast<int64_t>(b) * a.ngroups + g) * a.dstate + n0, Cv);
+  if constexpr (A_PER_STATE) {
+    float Av[V];
+    load_floats<V>(a.A + static_cast<int64_t>(hh) * a.dstate + n0, Av);
 #pragma unroll
-  for (int j = 0; j < CPT_ROWS; ++j) {
-    const int64_t q = (static_cast<int64_t>(blockIdx.x) * CPT_ROWS + j) * 256 + t;
-    const bool live = q < a.n_chunks;  // whole rows are live or dead together
-    const int64_t qq = live ? q : 0;
-    const int64_t e = qq * V;
-    const int64_t row = e / a.dstate;
-    const int64_t bh = row / a.headdim;  // b * nheads + h
-    const int hh = static_cast<int>(bh % a.nheads);
-    const int64_t b = bh / a.nheads;
-    const int g = hh / a.heads_per_group;
-    const uint4 raw = load_chunk<F>(a.state, e);
-    const float xv = a.x[row];
-    const float dtv = a.dt[bh];
-    const float Dv = a.D ? a.D[hh] : 0.0f;
-    float Bv[V], Cv[V];
-    load_floats<V>(a.B + (b * a.ngroups + g) * a.dstate + n0, Bv);
-    load_floats<V>(a.C + (b * a.ngroups + g) * a.dstate + n0, Cv);
-    float dA[V];
-    if constexpr (A_PER_STATE) {
-      float Av[V];
-      load_floats<V>(a.A + static_cast<int64_t>(hh) * a.dstate + n0, Av);
+    for (int k = 0; k < V; ++k) dA[k] = decay(dtv, Av[k]);
+  } else {
+    const float d = decay(dtv, a.A[hh]);
 #pragma unroll
-      for (int k = 0; k < V; ++k) dA[k] = static_cast<float>(exp(static_cast<double>(dtv * Av[k])));
-    } else {
-      const float d = static_cast<float>(exp(static_cast<double>(dtv * a.A[hh])));
-#pragma unroll
-      for (int k = 0; k < V; ++k) dA[k] = d;
-    }
-    float s256 = 0.0f;
-    if constexpr (F == kE4M3) s256 = a.scale[e / a.group] * 256.0f;
-    const float dx = dtv * xv;
-    float h[V];
-    float ys = 0.0f;
-#pragma unroll
-    for (int k = 0; k < V; ++k) {
-      const float hp = decode_code<F>(chunk_code<F>(raw, k), s256);
-      const float w = dx * Bv[k];
-      h[k] = fmaf(dA[k], hp, w);
-      ys = fmaf(Cv[k], h[k], ys);
-    }
-    ys = lane_sum(ys, a.lanes_per_row);
-    if (live && cc == 0) a.y[row] = ys + Dv * xv;
-    float r = 1.0f;
-    if constexpr (F == kE4M3) {
-      float m = 0.0f;
-#pragma unroll
-      for (int k = 0; k < V; ++k) m = fmaxf(m, fabsf(h[k]));
-      m = lane_max(m, a.lanes_per_group);
-      const float s = e4m3_scale(m);
-      r = (s == 0.0f) ? 0.0f : 1.0f / s;
-      if (live && (t & (a.lanes_per_group - 1)) == 0) a.scale[e / a.group] = s;
-    }
-    if (live) {
-      const uint4 out = quantize_chunk<F, R>(h, r, a.entry_base + static_cast<uint64_t>(e), a.thr);
-      store_chunk<F>(a.state, e, out);
-    }
+    for (int k = 0; k < V; ++k) dA[k] = d;
   }
+  float s_old = 1.0f;
+  if constexpr (F == kE4M3) s_old = a.scale[e >> a.group_shift];
+  float hp[V], h[V];
+  decode_chunk<F>(raw, s_old, hp);
+  const float dx = dtv * xv;
+  float ys = 0.0f;
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    const float w = dx * Bv[k];
+    h[k] = fmaf(dA[k], hp[k], w);
+    ys = fmaf(Cv[k], h[k], ys);
+  }
+  const bool bad = !__builtin_isfinite(ys);
+  ys = lane_sum(ys, a.lanes_per_row);
+  if (live && cc == 0) a.y[row] = ys + Dv * xv;
+  if constexpr (F == kE4M3) {
+    float m = 0.0f;
+#pragma unroll
+    for (int k = 0; k < V; ++k) m = fmaxf(m, __builtin_fabsf(h[k]));
+    const float s = e4m3_scale(__uint_as_float(lane_umax(__float_as_uint(m), a.lanes_per_group)));
+    const float rs = (s == 0.0f) ? 0.0f : 1.0f / s;
+    if (live && (t & (a.lanes_per_group - 1)) == 0) a.scale[e >> a.group_shift] = s;
+#pragma unroll
+    for (int k = 0; k < V; ++k) h[k] *= rs;
+  }
+  const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff, bad);
+  if (live) store_stream(state + e * Traits<F>::bytes, out);
 }
 
 // ---------------------------------------------------------------------------
-// Requantize (no scale): 16 entries per thread; the last partial chunk entry by entry.
+// Requantize without scale: one chunk of V entries per thread; the entries
+// after the last whole chunk one by one.
 // ---------------------------------------------------------------------------
+template <int F>
+__device__ inline void store_code(void* codes, int64_t k, uint32_t c) {
+  if constexpr (Traits<F>::bytes == 2) static_cast<uint16_t*>(codes)[k] = static_cast<uint16_t>(c);
+  else if constexpr (Traits<F>::bytes == 4) static_cast<uint32_t*>(codes)[k] = c;
+  else static_cast<uint8_t*>(codes)[k] = static_cast<uint8_t>(c);
+}
+
 template <int F, int R>
 __global__ __launch_bounds__(256) void k_requant(RequantArgs a) {
+  constexpr int V = Traits<F>::V;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  const int64_t e = q * 16;
+  const int64_t e = q * V;
   if (e >= a.n) return;
   const uint64_t ge = a.entry_base + static_cast<uint64_t>(e);
-  if (e + 16 <= a.n) {
-    float h[16];
-    load_floats<16>(a.h + e, h);
-    constexpr int V = Traits<F>::V;
-#pragma unroll
-    for (int part = 0; part < 16 / V; ++part) {
-      float hv[V];
-#pragma unroll
-      for (int k = 0; k < V; ++k) hv[k] = h[part * V + k];
-      const uint4 out = quantize_chunk<F, R>(hv, 1.0f, ge + part * V, a.thr);
-      store_chunk<F>(a.codes, e + part * V, out);
-    }
+  if (e + V <= a.n) {
+    float h[V];
+    load_floats<V>(a.h + e, h);
+    const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(ge, a.thr), a.toff, chunk_has_nan<V>(h));
+    *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + e * Traits<F>::bytes) = out;
   } else {
     for (int64_t k = e; k < a.n; ++k) {
       const uint64_t gk = a.entry_base + static_cast<uint64_t>(k);
-      const uint32_t c = round_code<F, R>(a.h[k], thr_word<R>(thr_base<R>(gk, a.thr), 0u, a.thr));
-      if constexpr (Traits<F>::bytes == 2) static_cast<uint16_t*>(a.codes)[k] = static_cast<uint16_t>(c);
-      else if constexpr (Traits<F>::bytes == 4) static_cast<uint32_t*>(a.codes)[k] = c;
-      else static_cast<uint8_t*>(a.codes)[k] = static_cast<uint8_t>(c);
+      store_code<F>(a.codes, k, round_code<F, R>(a.h[k], thr_word<R>(thr_base<R>(gk, a.thr), 0u)));
     }
   }
 }
@@ -284,7 +279,7 @@ __global__ __launch_bounds__(256) void k_requant(RequantArgs a) {
 // ---------------------------------------------------------------------------
 // Requantize to E4M3 with group scales. lanes_per_group lanes (a power of two
 // <= 64) work on one group; a wave covers 64 / lanes_per_group groups per
-// iteration and loops over the group's 16-entry chunks.
+// iteration and loops over each group's 16-entry chunks.
 // ---------------------------------------------------------------------------
 template <int R>
 __global__ __launch_bounds__(256) void k_requant_e4m3(RequantArgs a) {
@@ -306,21 +301,23 @@ __global__ __launch_bounds__(256) void k_requant_e4m3(RequantArgs a) {
         float h[16];
         load_floats<16>(a.h + grp * a.group + c * 16, h);
 #pragma unroll
-        for (int k = 0; k < 16; ++k) m = fmaxf(m, fabsf(h[k]));
+        for (int k = 0; k < 16; ++k) m = fmaxf(m, __builtin_fabsf(h[k]));
       }
     }
-    m = lane_max(m, LG);
-    const float s = e4m3_scale(m);
-    const float r = (s == 0.0f) ? 0.0f : 1.0f / s;
+    const float s = e4m3_scale(__uint_as_float(lane_umax(__float_as_uint(m), LG)));
+    const float rs = (s == 0.0f) ? 0.0f : 1.0f / s;
     if (live && li == 0) a.scale[grp] = s;
-    if (live) {
-      for (int64_t c = li; c < chunks_per_group; c += LG) {
-        const int64_t e = grp * a.group + c * 16;
-        float h[16];
-        load_floats<16>(a.h + e, h);
-        const uint4 out = quantize_chunk<kE4M3, R>(h, r, a.entry_base + static_cast<uint64_t>(e), a.thr);
-        store_chunk<kE4M3>(a.codes, e, out);
-      }
+    const int64_t iters = (chunks_per_group + LG - 1) / LG;  // uniform trip count
+    for (int64_t it = 0; it < iters; ++it) {
+      const int64_t c = it * LG + li;
+      const bool ok = live && c < chunks_per_group;
+      const int64_t e = (ok ? grp * a.group + c * 16 : 0);
+      float h[16];
+      load_floats<16>(a.h + e, h);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) h[k] *= rs;
+      const uint4 out = quantize_chunk<kE4M3, R>(h, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff, chunk_has_nan<16>(h));
+      if (ok) *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + e) = out;
     }
   }
 }
@@ -333,35 +330,38 @@ __global__ __launch_bounds__(256) void k_dither_fill(DitherArgs a) {
   const int64_t lim = (a.n - e < 4) ? (a.n - e) : 4;
   for (int64_t k = 0; k < lim; ++k) {
     const uint64_t ge = a.entry_base + static_cast<uint64_t>(e + k);
-    a.out[e + k] = (R == kRTN) ? (1u << 23) : (thr_word<R>(thr_base<R>(ge, a.thr), 0u, a.thr) >> 8);
+    a.out[e + k] = (R == kRTN) ? (1u << 23) : (thr_word<R>(thr_base<R>(ge, a.thr), 0u) >> 8);
   }
 }
 
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
-template <int F, int R, int CPT>
-static hipError_t launch_head_cpt(const UpdateArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((k_update_head<F, R, CPT>), dim3(static_cast<unsigned>(a.batch * a.nheads)),
-                     dim3(256), 0, s, a);
+template <int F, int R, int NT, int CPT>
+static hipError_t launch_slab(const UpdateArgs& a, hipStream_t s) {
+  const int64_t blocks = a.batch * a.nheads * a.slabs_per_head;
+  hipLaunchKernelGGL((k_update_slab<F, R, NT, CPT>), dim3(static_cast<unsigned>(blocks)), dim3(NT),
+                     0, s, a);
   return hipGetLastError();
 }
 
 template <int F, int R>
-static hipError_t launch_head_fr(const UpdateArgs& a, int cpt, hipStream_t s) {
-  switch (cpt) {
-    case 1: return launch_head_cpt<F, R, 1>(a, s);
-    case 2: return launch_head_cpt<F, R, 2>(a, s);
-    case 4: return launch_head_cpt<F, R, 4>(a, s);
-    case 8: return launch_head_cpt<F, R, 8>(a, s);
+static hipError_t launch_slab_cfg(const UpdateArgs& a, int cfg, hipStream_t s) {
+  switch (cfg) {
+    case kSlab256x1: return launch_slab<F, R, 256, 1>(a, s);
+    case kSlab256x2: return launch_slab<F, R, 256, 2>(a, s);
+    case kSlab256x4: return launch_slab<F, R, 256, 4>(a, s);
+    case kSlab512x2: return launch_slab<F, R, 512, 2>(a, s);
+    case kSlab512x4: return launch_slab<F, R, 512, 4>(a, s);
+    case kSlab1024x4: return launch_slab<F, R, 1024, 4>(a, s);
+    case kSlab1024x8: return launch_slab<F, R, 1024, 8>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int F, int R>
-static hipError_t launch_rows_fr(const UpdateArgs& a, bool a_per_state, hipStream_t s) {
-  const int64_t per_block = 256LL * CPT_ROWS;
-  const unsigned grid = static_cast<unsigned>((a.n_chunks + per_block - 1) / per_block);
+static hipError_t launch_rows(const UpdateArgs& a, bool a_per_state, hipStream_t s) {
+  const unsigned grid = static_cast<unsigned>((a.n_chunks + 255) / 256);
   if (a_per_state)
     hipLaunchKernelGGL((k_update_rows<F, R, true>), dim3(grid), dim3(256), 0, s, a);
   else
@@ -369,29 +369,34 @@ static hipError_t launch_rows_fr(const UpdateArgs& a, bool a_per_state, hipStrea
   return hipGetLastError();
 }
 
+template <int F, int R>
+static hipError_t launch_update_fr(const UpdateArgs& a, int cfg, bool aps, hipStream_t s) {
+  return cfg == kRowKernel ? launch_rows<F, R>(a, aps, s) : launch_slab_cfg<F, R>(a, cfg, s);
+}
+
 template <int F>
-static hipError_t dispatch_update_f(const UpdateArgs& a, int rule, int kind, int cpt, bool aps,
-                                    hipStream_t s) {
+static hipError_t launch_update_f(const UpdateArgs& a, int rule, int cfg, bool aps, hipStream_t s) {
   switch (rule) {
-    case kRTN: return kind == 0 ? launch_head_fr<F, kRTN>(a, cpt, s) : launch_rows_fr<F, kRTN>(a, aps, s);
-    case kSR: return kind == 0 ? launch_head_fr<F, kSR>(a, cpt, s) : launch_rows_fr<F, kSR>(a, aps, s);
-    default: return kind == 0 ? launch_head_fr<F, kWEYL>(a, cpt, s) : launch_rows_fr<F, kWEYL>(a, aps, s);
+    case kRTN: return launch_update_fr<F, kRTN>(a, cfg, aps, s);
+    case kSR: return launch_update_fr<F, kSR>(a, cfg, aps, s);
+    default: return launch_update_fr<F, kWEYL>(a, cfg, aps, s);
   }
 }
 
-hipError_t launch_update(const UpdateArgs& a, int format, int rule, int kind, int cpt,
-                         bool a_per_state, hipStream_t s) {
+hipError_t launch_update(const UpdateArgs& a, int format, int rule, int cfg, bool a_per_state,
+                         hipStream_t s) {
   switch (format) {
-    case kFP16: return dispatch_update_f<kFP16>(a, rule, kind, cpt, a_per_state, s);
-    case kBF16: return dispatch_update_f<kBF16>(a, rule, kind, cpt, a_per_state, s);
-    case kE4M3: return dispatch_update_f<kE4M3>(a, rule, kind, cpt, a_per_state, s);
-    default: return dispatch_update_f<kFP32>(a, rule, kind, cpt, a_per_state, s);
+    case kFP16: return launch_update_f<kFP16>(a, rule, cfg, a_per_state, s);
+    case kBF16: return launch_update_f<kBF16>(a, rule, cfg, a_per_state, s);
+    case kE4M3: return launch_update_f<kE4M3>(a, rule, cfg, a_per_state, s);
+    default: return launch_update_f<kFP32>(a, rule, cfg, a_per_state, s);
   }
 }
 
 template <int F>
 static hipError_t launch_requant_f(const RequantArgs& a, int rule, hipStream_t s) {
-  const int64_t chunks = (a.n + 15) / 16;
+  constexpr int V = Traits<F>::V;
+  const int64_t chunks = (a.n + V - 1) / V;
   const unsigned grid = static_cast<unsigned>((chunks + 255) / 256);
   switch (rule) {
     case kRTN: hipLaunchKernelGGL((k_requant<F, kRTN>), dim3(grid), dim3(256), 0, s, a); break;

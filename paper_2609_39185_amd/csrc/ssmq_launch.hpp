@@ -13,6 +13,40 @@ struct Thr {
   uint32_t lb;   // log2(dither_block)
 };
 
+// Division of 32-bit unsigned integers by an invariant d >= 1 with one high
+// multiply (Granlund and Montgomery, "Division by invariant integers using
+// multiplication", 1994, Figure 4.1): with l = ceil(log2 d),
+// m = floor(2^32 (2^l - d) / d) + 1, t = mulhi(m, n),
+// n / d = (t + ((n - t) >> sh1)) >> sh2, sh1 = min(l, 1), sh2 = max(l - 1, 0).
+struct FastDiv {
+  uint32_t d, m, sh1, sh2;
+  __host__ __device__ uint32_t div(uint32_t n) const {
+    const uint32_t t = static_cast<uint32_t>((static_cast<uint64_t>(m) * n) >> 32);
+    return (t + ((n - t) >> sh1)) >> sh2;
+  }
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((uint64_t{1} << l) < d) ++l;
+  FastDiv f;
+  f.d = d;
+  f.m = static_cast<uint32_t>(((uint64_t{1} << 32) * ((uint64_t{1} << l) - d)) / d + 1);
+  f.sh1 = l < 1 ? l : 1;
+  f.sh2 = l > 1 ? l - 1 : 0;
+  return f;
+}
+
+// Launch configurations of the update: slab kernels (threads x chunks per
+// thread) and the row kernel.
+enum UpdateConfig : int {
+  kSlab256x1 = 0, kSlab256x2, kSlab256x4, kSlab512x2, kSlab512x4, kSlab1024x4, kSlab1024x8,
+  kRowKernel
+};
+constexpr int kSlabThreads[] = {256, 256, 256, 512, 512, 1024, 1024};
+constexpr int kSlabChunks[] = {1, 2, 4, 2, 4, 4, 8};
+constexpr int kMaxDstate = 1024;  // 64 lanes x 16 E4M3 entries per row
+
 struct UpdateArgs {
   void* state;
   float* scale;
@@ -28,12 +62,18 @@ struct UpdateArgs {
   int32_t heads_per_group;
   int32_t lanes_per_row;    // dstate / V, a power of two <= 64
   int32_t lr_shift;         // log2(lanes_per_row)
-  int32_t group;            // E4M3 entries per scale
-  int32_t lanes_per_group;  // E4M3: group / 16 lanes; 0 = one scale per head tile
+  int32_t dstate_shift;     // log2(dstate)
+  int32_t group_shift;      // E4M3: log2(entries per scale) when that is a power of two
+  int32_t lanes_per_group;  // E4M3: group / 16 lanes; 0 = one scale per head slab
+  int32_t slabs_per_head;   // slab kernels: workgroups per (batch, head) tile
   int64_t head_size;        // headdim * dstate
   int64_t n_chunks;         // total entries / V
   uint64_t entry_base;
   Thr thr;
+  uint32_t toff[16];        // threshold offset of entry k of a chunk
+  uint32_t pass_thr_inc;    // slab kernels: threshold base increment per pass ...
+  int32_t pass_thr_ok;      // ... when a pass advances by whole dither blocks (or SR)
+  FastDiv div_headdim, div_nheads, div_hpg, div_slabs;  // index arithmetic
 };
 
 struct RequantArgs {
@@ -45,6 +85,7 @@ struct RequantArgs {
   int32_t lanes_per_group;  // E4M3 lanes cooperating on one group
   uint64_t entry_base;
   Thr thr;
+  uint32_t toff[16];
 };
 
 struct DitherArgs {
@@ -54,9 +95,8 @@ struct DitherArgs {
   Thr thr;
 };
 
-// kind 0: head-tile kernel with `cpt` chunks per thread; kind 1: row kernel.
-hipError_t launch_update(const UpdateArgs& a, int format, int rule, int kind, int cpt,
-                         bool a_per_state, hipStream_t s);
+hipError_t launch_update(const UpdateArgs& a, int format, int rule, int cfg, bool a_per_state,
+                         hipStream_t s);
 hipError_t launch_requant(const RequantArgs& a, int format, int rule, hipStream_t s);
 hipError_t launch_dither(const DitherArgs& a, int rule, hipStream_t s);
 

@@ -67,7 +67,8 @@ def _edge_values(fmt, rng, n_random, entry_base, rule, block, seed, layer, step)
     lo = oracle.decode(fmt, oracle.round_values(fmt, "weyl", x, np.zeros_like(U)))
     hi = oracle.decode(fmt, oracle.round_values(fmt, "weyl", x, np.full_like(U, TWO24 - 1)))
     ok = np.isfinite(lo) & np.isfinite(hi) & (hi != lo) & (rng.random(x.size) < 0.3)
-    pt = hi - (U / TWO24) * (hi - lo)
+    with np.errstate(invalid="ignore"):
+        pt = np.where(ok, hi - (U / TWO24) * (hi - lo), 0.0)
     p32 = pt.astype(np.float32)
     sel = np.nonzero(ok)[0]
     jitter = rng.integers(-1, 2, sel.size)
