@@ -18,12 +18,13 @@
  *
  * Floating-point order of the fused step (fp32, no contraction; this file must
  * be compiled with -ffp-contract=off):
- *   h_prev = decode(code)                    (x s_old for fp8, one fp32 product)
  *   z      = fl32(dt * A)
  *   dA     = fl32(exp(z))                    (exp in double, then one rounding)
  *   dx     = fl32(dt * x_p)
  *   w      = fl32(dx * B_n)
- *   h_new  = fma(dA, h_prev, w)              (one rounding)
+ *   h_new  = fma(dA, h_prev, w)              (one rounding), h_prev = decode(code)
+ *            E4M3: the stored value is v * s_old (v the exact code value), and
+ *            dA * (v * s_old) is taken as fma(fl32(dA * s_old), v, w)
  *   y_p    = sum_n C_n h_new + D x_p         (accumulated in double)
  * then h_new is written back under the chosen rounding rule.
  */
@@ -364,12 +365,10 @@ static void store_code(int f, void *p, int64_t k, uint32_t c) {
     }
 }
 
-/* Stored code -> fp32 value; for E4M3 one fp32 product with the group scale. */
-static float dequantize(int f, uint32_t code, float scale) {
+/* Stored code -> its exact value as fp32 (E4M3: without the group scale). */
+static float code_value(int f, uint32_t code) {
     if (f == ORC_FP32) return bits_f32(code);
-    float v = (float)decode_fields(f, code); /* exact: every code is an fp32 value */
-    if (f == ORC_E4M3) v = v * scale;
-    return v;
+    return (float)decode_fields(f, code); /* exact: every code is an fp32 value */
 }
 
 /*
@@ -475,11 +474,15 @@ int orc_state_update(int f, int rule, uint32_t seed, uint32_t layer, uint32_t st
                     const float a = a_per_state ? A[hd * dstate + n] : A[hd];
                     const float z = dtv * a;
                     const float dA = (float)exp((double)z);
-                    float s_old = 0.0f;
-                    if (f == ORC_E4M3) s_old = scale[k / group];
-                    const float hp = dequantize(f, load_code(f, state, k), s_old);
+                    const float v = code_value(f, load_code(f, state, k));
                     const float w = dx * Bg[n];
-                    const float h_new = fmaf(dA, hp, w);
+                    float h_new;
+                    if (f == ORC_E4M3) {
+                        const float dAs = dA * scale[k / group]; /* decay times old scale */
+                        h_new = fmaf(dAs, v, w);
+                    } else {
+                        h_new = fmaf(dA, v, w);
+                    }
                     hn[k] = h_new;
                     acc += (double)Cg[n] * (double)h_new;
                 }

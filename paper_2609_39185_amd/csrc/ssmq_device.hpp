@@ -246,9 +246,12 @@ __device__ inline bool chunk_has_nan(const float (&v)[V]) {
   return n;
 }
 
+// may_saturate: some |v| of the chunk may exceed 448 (E4M3); the clamp then runs
+// in a wave-uniform branch (a chunk's max|v| <= 448 implies every |v| <= 448).
 template <int F, int R>
 __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t base,
-                                       const uint32_t* off, bool maybe_nan) {
+                                       const uint32_t* off, bool maybe_nan,
+                                       bool may_saturate = true) {
   constexpr int V = Traits<F>::V;
   uint32_t w[4];
   if constexpr (F == kFP32) {
@@ -263,7 +266,9 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
       if constexpr (R == kRTN) {
         p = (v2bf){static_cast<__bf16>(v[2 * i]), static_cast<__bf16>(v[2 * i + 1])};
       } else {
-        p = __builtin_amdgcn_cvt_sr_bf16_f32((v2bf){0, 0}, v[2 * i],
+        // the previous contents of the destination are don't-care: both halves are written
+        p = __builtin_bit_cast(v2bf, __float_as_uint(v[2 * i]));
+        p = __builtin_amdgcn_cvt_sr_bf16_f32(p, v[2 * i],
                                              signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]),
                                              false);
         p = __builtin_amdgcn_cvt_sr_bf16_f32(
@@ -278,7 +283,8 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
       if constexpr (R == kRTN) {
         p = (v2h){static_cast<_Float16>(v[2 * i]), static_cast<_Float16>(v[2 * i + 1])};
       } else {
-        p = __builtin_amdgcn_cvt_sr_f16_f32((v2h){0, 0}, v[2 * i],
+        p = __builtin_bit_cast(v2h, __float_as_uint(v[2 * i]));
+        p = __builtin_amdgcn_cvt_sr_f16_f32(p, v[2 * i],
                                             signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]),
                                             false);
         p = __builtin_amdgcn_cvt_sr_f16_f32(
@@ -286,18 +292,22 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
       }
       w[i] = __builtin_bit_cast(uint32_t, p);
     }
-  } else {  // E4M3, values already scaled; clamp = saturation at 448
+  } else {  // E4M3, values already scaled; saturation at 448 by clamping
     float q[V];
 #pragma unroll
-    for (int k = 0; k < V; ++k) q[k] = __builtin_amdgcn_fmed3f(v[k], -448.0f, 448.0f);
+    for (int k = 0; k < V; ++k) q[k] = v[k];
+    if (__builtin_amdgcn_ballot_w64(may_saturate) != 0) {
+#pragma unroll
+      for (int k = 0; k < V; ++k) q[k] = __builtin_amdgcn_fmed3f(q[k], -448.0f, 448.0f);
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      int d = 0;
+      const int k = 4 * i;
+      int d = static_cast<int>(__float_as_uint(q[k]));  // don't-care: all four bytes are written
       if constexpr (R == kRTN) {
-        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[4 * i], q[4 * i + 1], d, false);
-        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[4 * i + 2], q[4 * i + 3], d, true);
+        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k], q[k + 1], d, false);
+        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k + 2], q[k + 3], d, true);
       } else {
-        const int k = 4 * i;
         d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k], signed_thr(thr_word<R>(base, off[k]), q[k]), d, 0);
         d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 1], signed_thr(thr_word<R>(base, off[k + 1]), q[k + 1]), d, 1);
         d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 2], signed_thr(thr_word<R>(base, off[k + 2]), q[k + 2]), d, 2);
@@ -316,11 +326,11 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
 }
 
 // ---------------------------------------------------------------------------
-// Decoding code -> fp32 (exact; E4M3 through v_cvt_pk_f32_fp8, which decodes
-// OCP E4M3 exactly) and the group-scale product for E4M3.
+// Decoding code -> its exact value as fp32 (E4M3 without the group scale, via
+// v_cvt_pk_f32_fp8, which decodes OCP E4M3 exactly).
 // ---------------------------------------------------------------------------
 template <int F>
-__device__ inline void decode_chunk(const uint4& raw, float s, float (&out)[Traits<F>::V]) {
+__device__ inline void decode_chunk(const uint4& raw, float (&out)[Traits<F>::V]) {
   const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -334,10 +344,10 @@ __device__ inline void decode_chunk(const uint4& raw, float s, float (&out)[Trai
     } else if constexpr (F == kE4M3) {
       const v2f lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), false);
       const v2f hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), true);
-      out[4 * i] = lo.x * s;
-      out[4 * i + 1] = lo.y * s;
-      out[4 * i + 2] = hi.x * s;
-      out[4 * i + 3] = hi.y * s;
+      out[4 * i] = lo.x;
+      out[4 * i + 1] = lo.y;
+      out[4 * i + 2] = hi.x;
+      out[4 * i + 3] = hi.y;
     } else {
       out[i] = __uint_as_float(w[i]);
     }

@@ -56,16 +56,20 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
   const int rows_per_pass = NT >> a.lr_shift;
   const int r0 = (t >> a.lr_shift) + static_cast<int>(slab) * rows_per_pass * CPT;
   const int64_t tile_base = tile * a.head_size;
-  const int64_t e0 = tile_base + static_cast<int64_t>(r0) * a.dstate + n0;  // first chunk
-  const int64_t pass = static_cast<int64_t>(rows_per_pass) * a.dstate;       // entries per pass
-  uint8_t* const state = static_cast<uint8_t*>(a.state);
+  // Uniform bases plus 32-bit lane offsets (a head holds fewer than 2^31 bytes).
+  uint8_t* const hstate = static_cast<uint8_t*>(a.state) + tile_base * Traits<F>::bytes;
+  const float* const hx = a.x + tile * a.headdim;
+  float* const hy = a.y + tile * a.headdim;
+  const uint32_t l0 = static_cast<uint32_t>(r0 * a.dstate + n0);  // lane's first entry in the head
+  const uint32_t pass = static_cast<uint32_t>(rows_per_pass * a.dstate);  // entries per pass
+  const int64_t e0 = tile_base + l0;
 
   uint4 raw[CPT];
   float xv[CPT];
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    raw[j] = load_stream(state + (e0 + j * pass) * Traits<F>::bytes);
-    xv[j] = a.x[tile * a.headdim + r0 + j * rows_per_pass];
+    raw[j] = load_stream(hstate + (l0 + j * pass) * Traits<F>::bytes);
+    xv[j] = hx[r0 + j * rows_per_pass];
   }
   const float dtv = a.dt[tile];
   const float Dv = a.D ? a.D[hh] : 0.0f;
@@ -87,40 +91,44 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
   }
   __syncthreads();
   const float dA = sh[0];
-  float Bv[V], Cv[V];
-#pragma unroll
-  for (int i = 0; i < V / 4; ++i) {
-    const float4 bq = sBC[(n0 >> 2) + i];
-    const float4 cq = sBC[nq + (n0 >> 2) + i];
-    Bv[4 * i] = bq.x; Bv[4 * i + 1] = bq.y; Bv[4 * i + 2] = bq.z; Bv[4 * i + 3] = bq.w;
-    Cv[4 * i] = cq.x; Cv[4 * i + 1] = cq.y; Cv[4 * i + 2] = cq.z; Cv[4 * i + 3] = cq.w;
-  }
 
   float h[CPT][V];
   bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    float s_old = 1.0f;
+    // E4M3 stores v * s_old; dA * (v * s_old) is evaluated as fma(fl32(dA * s_old), v, w).
+    float dAj = dA;
     if constexpr (F == kE4M3)
-      s_old = (a.lanes_per_group == 0) ? a.scale[tile] : a.scale[(e0 + j * pass) >> a.group_shift];
+      dAj = dA * ((a.lanes_per_group == 0) ? a.scale[tile] : a.scale[(e0 + j * pass) >> a.group_shift]);
     float hp[V];
-    decode_chunk<F>(raw[j], s_old, hp);
+    decode_chunk<F>(raw[j], hp);
     const float dx = dtv * xv[j];
     float ys = 0.0f;
+    // B and C come from LDS four at a time, so they are not held in registers
+    // across passes.
 #pragma unroll
-    for (int k = 0; k < V; ++k) {
-      const float w = dx * Bv[k];
-      h[j][k] = fmaf(dA, hp[k], w);
-      ys = fmaf(Cv[k], h[j][k], ys);
+    for (int i = 0; i < V / 4; ++i) {
+      const float4 bq = sBC[(n0 >> 2) + i];
+      const float4 cq = sBC[nq + (n0 >> 2) + i];
+      const float bk[4] = {bq.x, bq.y, bq.z, bq.w};
+      const float ck[4] = {cq.x, cq.y, cq.z, cq.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int k = 4 * i + u;
+        const float w = dx * bk[u];
+        h[j][k] = fmaf(dAj, hp[k], w);
+        ys = fmaf(ck[u], h[j][k], ys);
+      }
     }
     bad[j] = !__builtin_isfinite(ys);
     ys = lane_sum(ys, a.lanes_per_row);
-    if (cc == 0) a.y[tile * a.headdim + r0 + j * rows_per_pass] = ys + Dv * xv[j];
+    if (cc == 0) hy[r0 + j * rows_per_pass] = ys + Dv * xv[j];
   }
 
   float r[CPT];
+  bool sat[CPT];  // E4M3: fl32(max|h| * r) > 448 somewhere in the chunk
 #pragma unroll
-  for (int j = 0; j < CPT; ++j) r[j] = 1.0f;
+  for (int j = 0; j < CPT; ++j) { r[j] = 1.0f; sat[j] = false; }
   if constexpr (F == kE4M3) {
     // Lane maxima of |h| ignore NaN and are >= 0, so the cross-lane maximum can
     // compare bit patterns as unsigned integers.
@@ -163,20 +171,22 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
         if ((t & (a.lanes_per_group - 1)) == 0) a.scale[(e0 + j * pass) >> a.group_shift] = s;
       }
     }
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) sat[j] = __uint_as_float(m[j]) * r[j] > 448.0f;
   }
 
   const uint32_t base0 = thr_base<R>(a.entry_base + static_cast<uint64_t>(e0), a.thr);
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    const int64_t e = e0 + j * pass;
+    const int64_t e = e0 + static_cast<int64_t>(j) * pass;
     float v[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) v[k] = (F == kE4M3) ? h[j][k] * r[j] : h[j][k];
     const uint32_t base = (j == 0) ? base0
                           : (a.pass_thr_ok ? base0 + static_cast<uint32_t>(j) * a.pass_thr_inc
                                            : thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr));
-    const uint4 out = quantize_chunk<F, R>(v, base, a.toff, bad[j]);
-    store_stream(state + e * Traits<F>::bytes, out);
+    const uint4 out = quantize_chunk<F, R>(v, base, a.toff, bad[j], sat[j]);
+    store_stream(hstate + (l0 + j * pass) * Traits<F>::bytes, out);
   }
 }
 
@@ -216,10 +226,13 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
 #pragma unroll
     for (int k = 0; k < V; ++k) dA[k] = d;
   }
-  float s_old = 1.0f;
-  if constexpr (F == kE4M3) s_old = a.scale[e >> a.group_shift];
+  if constexpr (F == kE4M3) {  // fold the old group scale into the decay (see k_update_slab)
+    const float s_old = a.scale[e >> a.group_shift];
+#pragma unroll
+    for (int k = 0; k < V; ++k) dA[k] = dA[k] * s_old;
+  }
   float hp[V], h[V];
-  decode_chunk<F>(raw, s_old, hp);
+  decode_chunk<F>(raw, hp);
   const float dx = dtv * xv;
   float ys = 0.0f;
 #pragma unroll
