@@ -162,13 +162,14 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
 
   // Slab kernels for per-head A: a workgroup owns whole rows of one head, two
   // 16-byte chunks per thread; with one E4M3 scale per head the workgroup owns
-  // the whole head.
+  // the whole head, four chunks per thread (fewer, fuller threads amortise the
+  // per-workgroup scale reduction and its barriers).
   int cfg = -1;
   const int64_t head_chunks = head_size / V;
   if (d.a_per_state == 0 && fp8 && group == head_size) {
     switch (head_chunks) {
-      case 256: cfg = ssmq::kSlab256x1; break;
-      case 512: cfg = ssmq::kSlab256x2; break;
+      case 256: cfg = ssmq::kSlab64x4; break;
+      case 512: cfg = ssmq::kSlab128x4; break;
       case 1024: cfg = ssmq::kSlab256x4; break;
       case 2048: cfg = ssmq::kSlab512x4; break;
       case 4096: cfg = ssmq::kSlab1024x4; break;

@@ -210,8 +210,9 @@ __device__ inline void patch_code(uint32_t (&w)[4], int k, uint32_t c) {
 template <int F, int R>
 __device__ inline bool needs_exact_path(float v) {
   if constexpr (F == kE4M3) {
-    if constexpr (R == kRTN) return v != v;                            // NaN
-    else return !(__builtin_fabsf(v) >= 0x1p-10f);                     // NaN or k > 24
+    const float m = __builtin_fabsf(v);
+    if constexpr (R == kRTN) return !(m <= 448.0f);                    // NaN or saturation
+    else return !(m >= 0x1p-10f && m <= 448.0f);                      // NaN, k > 24, saturation
   } else if constexpr (F == kFP16) {
     if constexpr (R == kRTN) return false;
     else return __builtin_fabsf(v) < 0x1p-14f;                         // subnormal range
@@ -220,20 +221,21 @@ __device__ inline bool needs_exact_path(float v) {
   }
 }
 
-// Does any value of the chunk need the exact path? maybe_nan comes from the
-// caller (a NaN anywhere in the chunk, possibly a false alarm); the magnitude
-// tests use the chunk minimum (fminf ignores NaN).
+// Does any value of the chunk need the exact path? maybe_nan and may_saturate
+// come from the caller (a NaN, or for E4M3 a magnitude above 448, anywhere in
+// the chunk; either may be a false alarm); the small-magnitude tests use the
+// chunk minimum (fminf ignores NaN).
 template <int F, int R, int V>
-__device__ inline bool chunk_is_rare(const float (&v)[V], bool maybe_nan) {
+__device__ inline bool chunk_is_rare(const float (&v)[V], bool maybe_nan, bool may_saturate) {
   if constexpr (F == kBF16 || F == kFP32) return false;
   else if constexpr (F == kFP16 && R == kRTN) return false;
-  else if constexpr (F == kE4M3 && R == kRTN) return maybe_nan;
+  else if constexpr (F == kE4M3 && R == kRTN) return maybe_nan || may_saturate;
   else {
     float mn = __builtin_fabsf(v[0]);
 #pragma unroll
     for (int k = 1; k < V; ++k) mn = fminf(mn, __builtin_fabsf(v[k]));
     if constexpr (F == kFP16) return mn < 0x1p-14f;
-    else return maybe_nan || !(mn >= 0x1p-10f);
+    else return maybe_nan || may_saturate || !(mn >= 0x1p-10f);
   }
 }
 
@@ -246,12 +248,13 @@ __device__ inline bool chunk_has_nan(const float (&v)[V]) {
   return n;
 }
 
-// may_saturate: some |v| of the chunk may exceed 448 (E4M3); the clamp then runs
-// in a wave-uniform branch (a chunk's max|v| <= 448 implies every |v| <= 448).
+// may_saturate (E4M3): some |v| of the chunk may exceed 448. Such entries are
+// rare (the scale maps the group maximum to 448, so only its rounding error can
+// push a value past it) and take the exact path, which saturates; the
+// conversion instructions themselves do not.
 template <int F, int R>
 __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t base,
-                                       const uint32_t* off, bool maybe_nan,
-                                       bool may_saturate = true) {
+                                       const uint32_t* off, bool maybe_nan, bool may_saturate) {
   constexpr int V = Traits<F>::V;
   uint32_t w[4];
   if constexpr (F == kFP32) {
@@ -266,11 +269,10 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
       if constexpr (R == kRTN) {
         p = (v2bf){static_cast<__bf16>(v[2 * i]), static_cast<__bf16>(v[2 * i + 1])};
       } else {
-        // the previous contents of the destination are don't-care: both halves are written
-        p = __builtin_bit_cast(v2bf, __float_as_uint(v[2 * i]));
-        p = __builtin_amdgcn_cvt_sr_bf16_f32(p, v[2 * i],
-                                             signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]),
-                                             false);
+        // Both halves are written, so the destination's previous contents are
+        // don't-care: it starts as the first threshold, which dies here.
+        const uint32_t t0 = signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]);
+        p = __builtin_amdgcn_cvt_sr_bf16_f32(__builtin_bit_cast(v2bf, t0), v[2 * i], t0, false);
         p = __builtin_amdgcn_cvt_sr_bf16_f32(
             p, v[2 * i + 1], signed_thr(thr_word<R>(base, off[2 * i + 1]), v[2 * i + 1]), true);
       }
@@ -283,32 +285,25 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
       if constexpr (R == kRTN) {
         p = (v2h){static_cast<_Float16>(v[2 * i]), static_cast<_Float16>(v[2 * i + 1])};
       } else {
-        p = __builtin_bit_cast(v2h, __float_as_uint(v[2 * i]));
-        p = __builtin_amdgcn_cvt_sr_f16_f32(p, v[2 * i],
-                                            signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]),
-                                            false);
+        const uint32_t t0 = signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]);
+        p = __builtin_amdgcn_cvt_sr_f16_f32(__builtin_bit_cast(v2h, t0), v[2 * i], t0, false);
         p = __builtin_amdgcn_cvt_sr_f16_f32(
             p, v[2 * i + 1], signed_thr(thr_word<R>(base, off[2 * i + 1]), v[2 * i + 1]), true);
       }
       w[i] = __builtin_bit_cast(uint32_t, p);
     }
-  } else {  // E4M3, values already scaled; saturation at 448 by clamping
-    float q[V];
-#pragma unroll
-    for (int k = 0; k < V; ++k) q[k] = v[k];
-    if (__builtin_amdgcn_ballot_w64(may_saturate) != 0) {
-#pragma unroll
-      for (int k = 0; k < V; ++k) q[k] = __builtin_amdgcn_fmed3f(q[k], -448.0f, 448.0f);
-    }
+  } else {  // E4M3, values already scaled
+    const float (&q)[V] = v;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int k = 4 * i;
-      int d = static_cast<int>(__float_as_uint(q[k]));  // don't-care: all four bytes are written
+      int d;  // all four bytes are written: the previous contents are don't-care
       if constexpr (R == kRTN) {
-        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k], q[k + 1], d, false);
+        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k], q[k + 1], static_cast<int>(__float_as_uint(q[k])), false);
         d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k + 2], q[k + 3], d, true);
       } else {
-        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k], signed_thr(thr_word<R>(base, off[k]), q[k]), d, 0);
+        const uint32_t t0 = signed_thr(thr_word<R>(base, off[k]), q[k]);  // dies here
+        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k], t0, static_cast<int>(t0), 0);
         d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 1], signed_thr(thr_word<R>(base, off[k + 1]), q[k + 1]), d, 1);
         d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 2], signed_thr(thr_word<R>(base, off[k + 2]), q[k + 2]), d, 2);
         d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 3], signed_thr(thr_word<R>(base, off[k + 3]), q[k + 3]), d, 3);
@@ -316,7 +311,7 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
       w[i] = static_cast<uint32_t>(d);
     }
   }
-  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, V>(v, maybe_nan)) != 0) {
+  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, V>(v, maybe_nan, may_saturate)) != 0) {
 #pragma unroll
     for (int k = 0; k < V; ++k) {
       if (needs_exact_path<F, R>(v[k])) patch_code<F>(w, k, round_code<F, R>(v[k], thr_word<R>(base, off[k])));

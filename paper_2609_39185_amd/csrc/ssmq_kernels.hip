@@ -244,6 +244,7 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   const bool bad = !__builtin_isfinite(ys);
   ys = lane_sum(ys, a.lanes_per_row);
   if (live && cc == 0) a.y[row] = ys + Dv * xv;
+  bool sat = false;
   if constexpr (F == kE4M3) {
     float m = 0.0f;
 #pragma unroll
@@ -253,8 +254,9 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
     if (live && (t & (a.lanes_per_group - 1)) == 0) a.scale[e >> a.group_shift] = s;
 #pragma unroll
     for (int k = 0; k < V; ++k) h[k] *= rs;
+    sat = m * rs > 448.0f;  // rounding is monotone: the chunk maximum decides
   }
-  const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff, bad);
+  const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff, bad, sat);
   if (live) store_stream(state + e * Traits<F>::bytes, out);
 }
 
@@ -279,7 +281,7 @@ __global__ __launch_bounds__(256) void k_requant(RequantArgs a) {
   if (e + V <= a.n) {
     float h[V];
     load_floats<V>(a.h + e, h);
-    const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(ge, a.thr), a.toff, chunk_has_nan<V>(h));
+    const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(ge, a.thr), a.toff, chunk_has_nan<V>(h), false);
     *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + e * Traits<F>::bytes) = out;
   } else {
     for (int64_t k = e; k < a.n; ++k) {
@@ -327,9 +329,14 @@ __global__ __launch_bounds__(256) void k_requant_e4m3(RequantArgs a) {
       const int64_t e = (ok ? grp * a.group + c * 16 : 0);
       float h[16];
       load_floats<16>(a.h + e, h);
+      float mc = 0.0f;
 #pragma unroll
-      for (int k = 0; k < 16; ++k) h[k] *= rs;
-      const uint4 out = quantize_chunk<kE4M3, R>(h, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff, chunk_has_nan<16>(h));
+      for (int k = 0; k < 16; ++k) {
+        mc = fmaxf(mc, __builtin_fabsf(h[k]));
+        h[k] *= rs;
+      }
+      const uint4 out = quantize_chunk<kE4M3, R>(h, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff,
+                                                 chunk_has_nan<16>(h), mc * rs > 448.0f);
       if (ok) *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + e) = out;
     }
   }
@@ -361,6 +368,8 @@ static hipError_t launch_slab(const UpdateArgs& a, hipStream_t s) {
 template <int F, int R>
 static hipError_t launch_slab_cfg(const UpdateArgs& a, int cfg, hipStream_t s) {
   switch (cfg) {
+    case kSlab64x4: return launch_slab<F, R, 64, 4>(a, s);
+    case kSlab128x4: return launch_slab<F, R, 128, 4>(a, s);
     case kSlab256x1: return launch_slab<F, R, 256, 1>(a, s);
     case kSlab256x2: return launch_slab<F, R, 256, 2>(a, s);
     case kSlab256x4: return launch_slab<F, R, 256, 4>(a, s);

@@ -40,11 +40,11 @@ inline FastDiv make_fastdiv(uint32_t d) {
 // Launch configurations of the update: slab kernels (threads x chunks per
 // thread) and the row kernel.
 enum UpdateConfig : int {
-  kSlab256x1 = 0, kSlab256x2, kSlab256x4, kSlab512x2, kSlab512x4, kSlab1024x4, kSlab1024x8,
-  kRowKernel
+  kSlab64x4 = 0, kSlab128x4, kSlab256x1, kSlab256x2, kSlab256x4, kSlab512x2, kSlab512x4,
+  kSlab1024x4, kSlab1024x8, kRowKernel
 };
-constexpr int kSlabThreads[] = {256, 256, 256, 512, 512, 1024, 1024};
-constexpr int kSlabChunks[] = {1, 2, 4, 2, 4, 4, 8};
+constexpr int kSlabThreads[] = {64, 128, 256, 256, 256, 512, 512, 1024, 1024};
+constexpr int kSlabChunks[] = {4, 4, 1, 2, 4, 2, 4, 4, 8};
 constexpr int kMaxDstate = 1024;  // 64 lanes x 16 E4M3 entries per row
 
 struct UpdateArgs {
