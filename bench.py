@@ -23,6 +23,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, vendor figure
+CAL_ELEMS = 1 << 28      # calibration kernel: fp32 elements in and out
+CAL_BYTES = CAL_ELEMS * 4
+KERNEL_SOURCES = ("ssmq_kernels.hip", "ssmq_device.hpp", "ssmq_launch.hpp", "ssmq_abi.cpp")
+PROFILE_DIR = os.path.join(ROOT, "profiles")
 METRIC = "quantized state-update HBM GB/s (state R+W) & % of peak; decode steps/s"
 
 
@@ -37,7 +41,11 @@ def parse_args():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
-    ap.add_argument("--no-copy", action="store_true", help="skip the copy-bandwidth ceiling")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the streaming-kernel bandwidth ceiling")
+    ap.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                    help="turn rocprofv3 CSV output (kernel trace with --stats, then --pmc "
+                         "FETCH_SIZE, then --pmc WRITE_SIZE) into the summaries under profiles/")
     return ap.parse_args()
 
 
@@ -47,6 +55,8 @@ def state_bytes_per_entry(fmt: str) -> float:
 
 def main() -> int:
     args = parse_args()
+    if args.summarize_profiles:
+        return summarize_profiles(args.workload, *args.summarize_profiles)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build measures one GPU only; the state update shards "
@@ -127,25 +137,27 @@ def main() -> int:
             "state_bytes_per_launch": sbytes,
         }
 
-    # ---- copy ceiling: read + write the same bytes as one bf16 layer -----------------
-    copy = None
-    if not args.no_copy:
-        nbytes = n_entries * 2
-        src = torch.empty(nbytes // 4, dtype=torch.int32, device=dev).random_()
+    # ---- streaming ceiling: a plain elementwise kernel of known size ----------------
+    # torch.neg over 1 GiB of fp32 reads 1 GiB and writes 1 GiB; it is also the
+    # kernel that calibrates the FETCH_SIZE / WRITE_SIZE counters.
+    ceiling = None
+    if not args.no_ceiling:
+        src = torch.empty(CAL_ELEMS, dtype=torch.float32, device=dev).uniform_()
         dst = torch.empty_like(src)
         for _ in range(3):
-            dst.copy_(src)
+            torch.neg(src, out=dst)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         reps = 20
         e0.record(stream)
         for _ in range(reps):
-            dst.copy_(src)
+            torch.neg(src, out=dst)
         e1.record(stream)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / reps
-        copy = {"bytes_read_plus_written": 2 * nbytes, "us": ms * 1e3,
-                "GBps": 2 * nbytes / (ms * 1e6)}
+        ceiling = {"kernel": "torch.neg fp32 (1 GiB read, 1 GiB written)",
+                   "bytes_read_plus_written": 2 * CAL_BYTES, "us": ms * 1e3,
+                   "GBps": 2 * CAL_BYTES / (ms * 1e6)}
         del src, dst
 
     # ---- CPU baseline: the oracle on a bounded sample of one layer -------------------
@@ -155,14 +167,19 @@ def main() -> int:
 
     head_fmt, head_rule = variants[0]
     head = results[f"{head_fmt}:{head_rule}"]
+    measured = load_traffic(w.name)
+    for key, r in results.items():
+        t = measured.get(key) if measured else None
+        r["hbm_traffic_bytes_per_launch"] = t["traffic_bytes"] if t else None
+        r["kernel"] = t["kernel"] if t else "k_update_slab"
     roof = {
         "bound": "hbm",
         "achieved": head["kernel_state_GBps"],
         "peak": PEAK_HBM_GBPS,
         "unit": "GB/s",
         "frac": head["kernel_state_GBps"] / PEAK_HBM_GBPS,
-        "traffic": None,
-        "kernel": "k_update_head",
+        "traffic": head["hbm_traffic_bytes_per_launch"],
+        "kernel": head["kernel"],
         "algorithmic_bytes_per_launch": head["state_bytes_per_launch"],
         "avg_launch_us": head["kernel_avg_us"],
     }
@@ -187,11 +204,178 @@ def main() -> int:
         "steps_per_s": head["steps_per_s"],
         "roofline": roof,
         "cpu_baseline": cpu,
-        "copy_ceiling": copy,
+        "stream_ceiling": ceiling,
         "variants": results,
     }
     print(json.dumps(line), flush=True)
     return 0
+
+
+def kernel_sources_digest() -> str:
+    """sha256 over the sources that decide which kernel runs and what it does."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_39185_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_path(workload: str) -> str:
+    return os.path.join(PROFILE_DIR, f"k_update_slab.{workload}.traffic.json")
+
+
+def load_traffic(workload: str):
+    """Measured HBM bytes per launch for each variant, if the counters were taken
+    on the kernels as they are now (else None)."""
+    try:
+        with open(traffic_path(workload)) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_sources_sha256") != kernel_sources_digest():
+        return None
+    return rec.get("variants")
+
+
+# rocprofv3 names the update kernels k_update_slab<F, R, NT, CPT> with these codes
+_FMT_CODE = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3}
+_RULE_CODE = {"rtn": 0, "sr": 1, "weyl": 2}
+
+
+def _csv_rows(d: str, suffix: str):
+    import csv
+    import glob
+
+    hits = sorted(glob.glob(os.path.join(d, "**", "*" + suffix), recursive=True))
+    if not hits:
+        raise SystemExit(f"no *{suffix} under {d}")
+    with open(hits[0], newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _variant_of(kernel_name: str):
+    import re
+
+    m = re.search(r"k_update_(?:slab|rows)<(\d+), (\d+)", kernel_name)
+    if not m:
+        return None
+    f = {v: k for k, v in _FMT_CODE.items()}[int(m.group(1))]
+    r = {v: k for k, v in _RULE_CODE.items()}[int(m.group(2))]
+    return f"{f}:{r}"
+
+
+def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str) -> int:
+    """Write profiles/k_update_slab.<workload>.{kernel_trace.md,traffic.md,traffic.json}.
+
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by what they read for
+    the calibration kernel (torch.neg over CAL_BYTES in, CAL_BYTES out).
+    """
+    import statistics
+    from collections import defaultdict
+
+    from paper_2609_39185_amd import workloads as wl
+
+    w = wl.WORKLOADS[workload]
+    os.makedirs(PROFILE_DIR, exist_ok=True)
+    stats = _csv_rows(trace_dir, "kernel_stats.csv")
+    trace = _csv_rows(trace_dir, "kernel_trace.csv")
+    dur = defaultdict(list)
+    for r in trace:
+        dur[r["Kernel_Name"]].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+
+    def counter(d, name):
+        vals = defaultdict(list)
+        for r in _csv_rows(d, "counter_collection.csv"):
+            if r["Counter_Name"] == name:
+                vals[(r["Kernel_Name"], int(r["Grid_Size"]))].append(float(r["Counter_Value"]))
+        return vals
+
+    fetch, write = counter(fetch_dir, "FETCH_SIZE"), counter(write_dir, "WRITE_SIZE")
+
+    def calib(vals):
+        c = [statistics.mean(v) for (k, g), v in vals.items() if "neg_kernel" in k]
+        if not c:
+            raise SystemExit("no calibration kernel dispatch in the counter output")
+        return CAL_BYTES / (max(c) * 1024.0)
+
+    f_fetch, f_write = calib(fetch), calib(write)
+    n_entries = w.entries_per_layer
+    variants = {}
+    for (k, g), v in fetch.items():
+        key = _variant_of(k)
+        if key is None:
+            continue
+        fmt = key.split(":")[0]
+        algo = n_entries * state_bytes_per_entry(fmt) * 2
+        if fmt == "e4m3":
+            algo += (n_entries // (w.scale_group or w.headdim * w.dstate)) * 8
+        fk = statistics.mean(v)
+        wk = statistics.mean(write.get((k, g), [float("nan")]))
+        traffic = fk * 1024.0 * f_fetch + wk * 1024.0 * f_write
+        variants[key] = {
+            "kernel": k.replace("void ", "").replace("(ssmq::UpdateArgs)", "").replace("ssmq::", ""),
+            "dispatches": len(v), "fetch_KiB": fk, "write_KiB": wk,
+            "traffic_bytes": traffic, "algorithmic_bytes": algo,
+            "traffic_over_algorithmic": traffic / algo,
+            "trace_avg_us": statistics.mean(dur[k]) / 1e3 if k in dur else None,
+        }
+    rec = {
+        "workload": workload,
+        "kernel_sources_sha256": kernel_sources_digest(),
+        "calibration": {"kernel": "torch.neg fp32", "bytes_in": CAL_BYTES, "bytes_out": CAL_BYTES,
+                        "fetch_scale": f_fetch, "write_scale": f_write},
+        "commands": PROFILE_COMMANDS,
+        "variants": dict(sorted(variants.items())),
+    }
+    with open(traffic_path(workload), "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+
+    lines = [f"# k_update_slab on {workload}: HBM traffic per launch", "",
+             "Commands (repository root as $R, run from /tmp with TMPDIR=/tmp):", ""]
+    lines += [f"    {c}" for c in PROFILE_COMMANDS.values()]
+    lines += ["", f"Calibration: torch.neg over {CAL_BYTES} B in and out reads "
+                  f"FETCH_SIZE x {f_fetch:.4f}, WRITE_SIZE x {f_write:.4f} of the true bytes.", "",
+              "| variant | kernel | FETCH KiB | WRITE KiB | traffic B | algorithmic B | ratio |",
+              "|---|---|---|---|---|---|---|"]
+    for key, r in rec["variants"].items():
+        lines.append(f"| {key} | `{r['kernel']}` | {r['fetch_KiB']:.0f} | {r['write_KiB']:.0f} | "
+                     f"{r['traffic_bytes']:.4g} | {r['algorithmic_bytes']} | "
+                     f"{r['traffic_over_algorithmic']:.4f} |")
+    with open(os.path.join(PROFILE_DIR, f"k_update_slab.{workload}.traffic.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+    lines = [f"# Kernel trace of the default bench run on {workload}", "",
+             "Command (repository root as $R, run from /tmp with TMPDIR=/tmp):", "",
+             f"    {PROFILE_COMMANDS['trace']}", "",
+             "| kernel | calls | avg us | min us | max us | total ms |", "|---|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:16]:
+        name = r["Name"]
+        if len(name) > 80:
+            name = name[:77] + "..."
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.2f} |")
+    with open(os.path.join(PROFILE_DIR, f"k_update_slab.{workload}.kernel_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps({k: round(v["traffic_over_algorithmic"], 4) for k, v in variants.items()}))
+    return 0
+
+
+PROFILE_COMMANDS = {
+    "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof_trace "
+             "-o run -- python3 $R/bench.py",
+    "fetch": "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv "
+             "-d $R/gpurun_out/prof_fetch -o run -- python3 $R/bench.py --steps 2 --warmup 1 "
+             "--cpu-seconds 0",
+    "write": "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv "
+             "-d $R/gpurun_out/prof_write -o run -- python3 $R/bench.py --steps 2 --warmup 1 "
+             "--cpu-seconds 0",
+    "summary": "python3 $R/bench.py --summarize-profiles $R/gpurun_out/prof_trace "
+               "$R/gpurun_out/prof_fetch $R/gpurun_out/prof_write",
+}
 
 
 def cpu_baseline(w, variant, target_s):

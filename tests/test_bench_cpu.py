@@ -1,0 +1,67 @@
+"""Host-side pieces of bench.py: the --gpus guard, the rocprofv3 summary and the
+rule that measured traffic is reported only for the kernels it was taken on."""
+import csv
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
+
+
+def _write_csv(path, rows):
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=list(rows[0].keys()))
+        w.writeheader()
+        w.writerows(rows)
+
+
+def test_profile_summary_scales_counters_by_the_calibration_kernel(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "PROFILE_DIR", str(tmp_path / "profiles"))
+    upd = "void ssmq::k_update_slab<1, 2, 256, 2>(ssmq::UpdateArgs)"
+    neg = "void at::native::vectorized_elementwise_kernel<4, at::native::neg_kernel_cuda>"
+    cal_kib = bench.CAL_BYTES / 1024.0
+    trace = tmp_path / "trace"
+    _write_csv(str(trace / "run_kernel_stats.csv"),
+               [{"Name": upd, "Calls": 2, "TotalDurationNs": 340000, "AverageNs": 170000,
+                 "MinNs": 169000, "MaxNs": 171000}])
+    _write_csv(str(trace / "run_kernel_trace.csv"),
+               [{"Kernel_Name": upd, "Start_Timestamp": 0, "End_Timestamp": 170000},
+                {"Kernel_Name": upd, "Start_Timestamp": 500000, "End_Timestamp": 670000}])
+    from paper_2609_39185_amd import workloads as wl
+    algo = wl.WORKLOADS["hybrid_m2_stack"].entries_per_layer * 4
+    for name, counter, cal_read, upd_read in (("fetch", "FETCH_SIZE", cal_kib / 2, algo / 2048.0),
+                                              ("write", "WRITE_SIZE", cal_kib, algo / 2048.0)):
+        _write_csv(str(tmp_path / name / "run_counter_collection.csv"),
+                   [{"Kernel_Name": neg, "Grid_Size": 1 << 26, "Counter_Name": counter,
+                     "Counter_Value": cal_read},
+                    {"Kernel_Name": upd, "Grid_Size": 1 << 20, "Counter_Name": counter,
+                     "Counter_Value": upd_read}])
+    assert bench.summarize_profiles("hybrid_m2_stack", str(trace), str(tmp_path / "fetch"),
+                                    str(tmp_path / "write")) == 0
+    rec = json.load(open(tmp_path / "profiles" / "k_update_slab.hybrid_m2_stack.traffic.json"))
+    v = rec["variants"]["bf16:weyl"]
+    assert rec["calibration"]["fetch_scale"] == pytest.approx(2.0)
+    assert rec["calibration"]["write_scale"] == pytest.approx(1.0)
+    # fetch read half the true bytes (scaled x2), write read them all: 1.5x the algorithmic bytes
+    assert v["traffic_bytes"] == pytest.approx(1.5 * algo)
+    assert v["trace_avg_us"] == pytest.approx(170.0)
+    assert v["kernel"] == "k_update_slab<1, 2, 256, 2>"
+    # the counters describe the kernels as they are: reported while the digest matches ...
+    assert bench.load_traffic("hybrid_m2_stack")["bf16:weyl"]["traffic_bytes"] == v["traffic_bytes"]
+    # ... and not once the sources differ
+    rec["kernel_sources_sha256"] = "0" * 64
+    json.dump(rec, open(tmp_path / "profiles" / "k_update_slab.hybrid_m2_stack.traffic.json", "w"))
+    assert bench.load_traffic("hybrid_m2_stack") is None
