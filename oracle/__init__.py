@@ -6,7 +6,9 @@ GPU library computes (see ``ssmq_oracle.c`` for the definitions and the
 floating-point order) and shares no code with it.
 
 Formats: "fp16", "bf16", "e4m3" (OCP E4M3FN with an fp32 group scale), "fp32"
-(unrounded). Rules: "rtn", "sr", "weyl".
+(unrounded), "int8" and "int4" (symmetric integers with an fp32 block scale; INT4
+packs two entries per byte, the even entry in the low nibble). Rules: "rtn",
+"sr", "weyl".
 
 Parity status: every function here is pinned by tests under ``tests/`` that use
 what the paper and the mathematics fix (worked values, closed forms, exact
@@ -22,9 +24,30 @@ import numpy as np
 
 from . import build_oracle
 
-FORMATS = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3}
+FORMATS = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3, "int8": 4, "int4": 5}
 RULES = {"rtn": 0, "sr": 1, "weyl": 2}
-CODE_DTYPE = {"fp16": np.uint16, "bf16": np.uint16, "e4m3": np.uint8, "fp32": np.uint32}
+CODE_DTYPE = {"fp16": np.uint16, "bf16": np.uint16, "e4m3": np.uint8, "fp32": np.uint32,
+              "int8": np.uint8, "int4": np.uint8}
+SCALED = ("e4m3", "int8", "int4")
+QMAX = {"e4m3": 448.0, "int8": 127.0, "int4": 7.0}
+
+
+def entries_per_code_word(fmt: str) -> int:
+    """Entries stored per element of the code array (2 for packed INT4)."""
+    return 2 if fmt == "int4" else 1
+
+
+def entry_codes(fmt: str, codes) -> np.ndarray:
+    """One code per entry: INT4 bytes are split into their two nibbles (even entry
+    in the low nibble); other formats are returned as they are."""
+    c = np.asarray(codes)
+    if fmt != "int4":
+        return c
+    b = c.astype(np.uint8).reshape(-1)
+    out = np.empty(b.size * 2, np.uint8)
+    out[0::2] = b & 0xF
+    out[1::2] = b >> 4
+    return out
 
 _lib = None
 
@@ -137,11 +160,12 @@ def requantize(fmt: str, rule: str, h, *, seed=0, layer=0, step=0, entry_base=0,
                group=0):
     """Codes (and E4M3 group scales) for fp32 values h."""
     h = _c(h, np.float32).ravel()
-    codes = np.zeros(h.size, CODE_DTYPE[fmt])
+    per = entries_per_code_word(fmt)
+    codes = np.zeros((h.size + per - 1) // per, CODE_DTYPE[fmt])
     scale = None
-    if fmt == "e4m3":
+    if fmt in SCALED:
         if group <= 0:
-            raise ValueError("e4m3 needs a positive group")
+            raise ValueError(f"{fmt} needs a positive group")
         scale = np.zeros(h.size // group, np.float32)
     rc = lib().orc_requantize(FORMATS[fmt], RULES[rule], seed & 0xFFFFFFFF, layer & 0xFFFFFFFF,
                               step & 0xFFFFFFFF, entry_base, block, h.size, group, _ptr(h),
@@ -159,20 +183,21 @@ def state_update(fmt: str, rule: str, state, scale, x, dt, A, B, C, D, *, seed=0
     """
     state = np.array(state, dtype=CODE_DTYPE[fmt], copy=True, order="C")
     batch, nheads, headdim, dstate = state.shape
+    dstate *= entries_per_code_word(fmt)
     B = _c(B, np.float32)
     ngroups = B.shape[1]
     A = _c(A, np.float32)
     if a_per_state is None:
         a_per_state = 1 if A.ndim == 2 else 0
     sc = None
-    if fmt == "e4m3":
+    if fmt in SCALED:
         sc = np.array(scale, dtype=np.float32, copy=True).ravel()
     x = _c(x, np.float32)
     dt = _c(dt, np.float32)
     C = _c(C, np.float32)
     D = None if D is None else _c(D, np.float32)
     y = np.zeros((batch, nheads, headdim), np.float64)
-    hnew = np.zeros(state.shape, np.float32)
+    hnew = np.zeros((batch, nheads, headdim, dstate), np.float32)
     rc = lib().orc_state_update(FORMATS[fmt], RULES[rule], seed & 0xFFFFFFFF, layer & 0xFFFFFFFF,
                                 step & 0xFFFFFFFF, entry_base, block, group, batch, nheads,
                                 headdim, dstate, ngroups, a_per_state, _ptr(state), _ptr(sc),
@@ -184,12 +209,16 @@ def state_update(fmt: str, rule: str, state, scale, x, dt, A, B, C, D, *, seed=0
 
 
 def dequantize(fmt: str, codes, scale=None, group=0) -> np.ndarray:
-    """fp32 values of stored codes (E4M3: times the group scale, one fp32 product)."""
+    """fp32 values of stored codes, one per entry (E4M3, INT8, INT4: times the group
+    scale, one fp32 product). Shape: the codes' shape, INT4's last axis doubled."""
     codes = np.asarray(codes)
     if fmt == "fp32":
         return codes.astype(np.uint32).view(np.float32).astype(np.float32)
-    v = decode(fmt, codes).astype(np.float32).ravel()
-    if fmt == "e4m3":
+    shape = codes.shape
+    if fmt == "int4":
+        shape = shape[:-1] + (2 * shape[-1],) if len(shape) else (2,)
+    v = decode(fmt, entry_codes(fmt, codes)).astype(np.float32).ravel()
+    if fmt in SCALED:
         s = np.repeat(np.asarray(scale, np.float32).ravel(), group)
         v = (v * s).astype(np.float32)
-    return v.reshape(codes.shape)
+    return v.reshape(shape)

@@ -23,8 +23,8 @@
  *   dx     = fl32(dt * x_p)
  *   w      = fl32(dx * B_n)
  *   h_new  = fma(dA, h_prev, w)              (one rounding), h_prev = decode(code)
- *            E4M3: the stored value is v * s_old (v the exact code value), and
- *            dA * (v * s_old) is taken as fma(fl32(dA * s_old), v, w)
+ *            E4M3 and INT8/INT4: the stored value is v * s_old (v the exact code
+ *            value), and dA * (v * s_old) is taken as fma(fl32(dA * s_old), v, w)
  *   y_p    = sum_n C_n h_new + D x_p         (accumulated in double)
  * then h_new is written back under the chosen rounding rule.
  */
@@ -37,7 +37,16 @@
 /* ------------------------------------------------------------------------- */
 /* Identifiers (the oracle's own numbering; the Python wrapper maps names).  */
 /* ------------------------------------------------------------------------- */
-enum { ORC_FP16 = 0, ORC_BF16 = 1, ORC_E4M3 = 2, ORC_FP32 = 3 };
+enum { ORC_FP16 = 0, ORC_BF16 = 1, ORC_E4M3 = 2, ORC_FP32 = 3, ORC_INT8 = 4, ORC_INT4 = 5 };
+#define ORC_NFMT 6
+
+/* Symmetric integer formats with a block scale (Section 2 "Low-precision
+ * storage"; Appendix B "Formats"): INTb stores integers in [-qmax, qmax],
+ * qmax = 2^(b-1) - 1, two's complement; INT4 packs two entries per byte, the
+ * even entry in the low nibble. */
+static int is_int(int f) { return f == ORC_INT8 || f == ORC_INT4; }
+static int int_qmax(int f) { return f == ORC_INT8 ? 127 : 7; }
+static int is_scaled(int f) { return f == ORC_E4M3 || is_int(f); }
 enum { ORC_RTN = 0, ORC_SR = 1, ORC_WEYL = 2 };
 
 /* ------------------------------------------------------------------------- */
@@ -213,6 +222,41 @@ static uint32_t round_to_format(int f, int rule, float xf, uint32_t U24) {
     return g->code[pick];
 }
 
+/*
+ * Round the scaled fp32 value q onto the integer lattice {-qmax, ..., qmax}:
+ * eq. (dither) with step 1, lo = floor(q) and hi = lo + 1 (exact in double, as
+ * is hi - u for a 24-bit u). Values are clamped to [-qmax, qmax] first
+ * (Appendix B "Formats"); the bounds are lattice points, so clamping before
+ * or after rounding gives the same integer. RTN: nearest, exact ties to the
+ * even integer (the same tie rule as the floating-point casts). NaN has no
+ * integer code and is stored as 0. Returns the signed integer.
+ */
+static int32_t round_to_int(int qmax, int rule, float qf, uint32_t U24) {
+    if (isnan(qf)) return 0;
+    double x = (double)qf;
+    if (x > qmax) x = qmax;
+    if (x < -qmax) x = -qmax;
+    double lo = floor(x);
+    if (lo == x) return (int32_t)lo;
+    double hi = lo + 1.0;
+    if (rule == ORC_RTN) {
+        double mid = lo + 0.5;
+        if (x < mid) return (int32_t)lo;
+        if (x > mid) return (int32_t)hi;
+        return (fmod(lo, 2.0) == 0.0) ? (int32_t)lo : (int32_t)hi;
+    }
+    double u = (double)U24 / 16777216.0;
+    return (x >= hi - u) ? (int32_t)hi : (int32_t)lo;
+}
+
+/* storage code of one integer entry (byte for INT8, nibble for INT4) and back */
+static uint32_t int_code(int f, int32_t k) { return (uint32_t)k & (f == ORC_INT8 ? 0xFFu : 0xFu); }
+static int32_t int_value(int f, uint32_t code) {
+    if (f == ORC_INT8) return (int32_t)(int8_t)(uint8_t)code;
+    code &= 0xFu;
+    return (code & 0x8u) ? (int32_t)code - 16 : (int32_t)code;
+}
+
 /* ------------------------------------------------------------------------- */
 /* Thresholds.                                                                */
 /* ------------------------------------------------------------------------- */
@@ -292,6 +336,12 @@ uint32_t orc_fmix32(uint32_t h) { return fmix32(h); }
 
 int orc_grid(int f, double *val, uint32_t *code, int cap) {
     ensure_init();
+    if (is_int(f)) {
+        const int q = int_qmax(f), n = 2 * q + 1;
+        if (val && code)
+            for (int i = 0; i < n && i < cap; ++i) { val[i] = i - q; code[i] = int_code(f, i - q); }
+        return n;
+    }
     if (f < 0 || f > 2) return -1;
     const grid_t *g = &GRID[f];
     if (val && code) {
@@ -303,12 +353,17 @@ int orc_grid(int f, double *val, uint32_t *code, int cap) {
 
 double orc_decode(int f, uint32_t code) {
     if (f == ORC_FP32) return (double)bits_f32(code);
+    if (is_int(f)) return (double)int_value(f, code);
     return decode_fields(f, code);
 }
 
 /* Position of a code in its format's value order (both zeros share one). */
 int orc_code_rank(int f, uint32_t code) {
     ensure_init();
+    if (is_int(f)) {
+        int32_t k = int_value(f, code);
+        return (k < -int_qmax(f)) ? -1 : k + int_qmax(f);  /* -128 / -8 are not codes */
+    }
     double v = decode_fields(f, code);
     if (isnan(v)) return -1;
     const grid_t *g = &GRID[f];
@@ -322,6 +377,7 @@ int orc_code_rank(int f, uint32_t code) {
 uint32_t orc_round(int f, int rule, float x, uint32_t U24) {
     ensure_init();
     if (f == ORC_FP32) return f32_bits(x);
+    if (is_int(f)) return int_code(f, round_to_int(int_qmax(f), rule, x, U24 & 0xFFFFFFu));
     return round_to_format(f, rule, x, U24 & 0xFFFFFFu);
 }
 
@@ -345,11 +401,15 @@ void orc_dither_fill(int rule, uint32_t seed, uint32_t layer, uint32_t step, uin
 }
 
 /* ------------------------------------------------------------------------- */
-/* Code storage helpers (codes are 1, 2 or 4 bytes per entry).               */
+/* Code storage helpers (codes are 1, 2 or 4 bytes per entry; INT4 packs two */
+/* entries per byte, entry 2j in the low nibble of byte j).                   */
 /* ------------------------------------------------------------------------- */
-static int code_bytes(int f) { return f == ORC_E4M3 ? 1 : (f == ORC_FP32 ? 4 : 2); }
+static int code_bytes(int f) {
+    return (f == ORC_E4M3 || is_int(f)) ? 1 : (f == ORC_FP32 ? 4 : 2);
+}
 
 static uint32_t load_code(int f, const void *p, int64_t k) {
+    if (f == ORC_INT4) return (((const uint8_t *)p)[k / 2] >> (4 * (k % 2))) & 0xFu;
     switch (code_bytes(f)) {
         case 1: return ((const uint8_t *)p)[k];
         case 2: return ((const uint16_t *)p)[k];
@@ -358,6 +418,12 @@ static uint32_t load_code(int f, const void *p, int64_t k) {
 }
 
 static void store_code(int f, void *p, int64_t k, uint32_t c) {
+    if (f == ORC_INT4) {
+        uint8_t *b = (uint8_t *)p + k / 2;
+        const int sh = 4 * (int)(k % 2);
+        *b = (uint8_t)((*b & ~(0xFu << sh)) | ((c & 0xFu) << sh));
+        return;
+    }
     switch (code_bytes(f)) {
         case 1: ((uint8_t *)p)[k] = (uint8_t)c; break;
         case 2: ((uint16_t *)p)[k] = (uint16_t)c; break;
@@ -368,16 +434,19 @@ static void store_code(int f, void *p, int64_t k, uint32_t c) {
 /* Stored code -> its exact value as fp32 (E4M3: without the group scale). */
 static float code_value(int f, uint32_t code) {
     if (f == ORC_FP32) return bits_f32(code);
+    if (is_int(f)) return (float)int_value(f, code);
     return (float)decode_fields(f, code); /* exact: every code is an fp32 value */
 }
 
 /*
  * Requantize n fp32 values into format f (Appendix B "Formats").
- * E4M3 uses one fp32 scale per group of `group` consecutive entries:
- *   m = max |h| over the group (NaN entries ignored), s = fl32(m / 448);
+ * E4M3 and INT8/INT4 use one fp32 scale per group of `group` consecutive
+ * entries, with qmax = 448 (E4M3), 127 (INT8) or 7 (INT4):
+ *   m = max |h| over the group (NaN entries ignored), s = fl32(m / qmax);
  *   s below the smallest normal fp32 is stored as 0 and every code is a
- *   signed zero (NaN stays NaN); otherwise r = fl32(1 / s) and each entry is
- *   rounded as q = fl32(h * r) on the E4M3 grid.
+ *   (signed, for E4M3) zero, NaN staying NaN in E4M3; otherwise r = fl32(1 / s)
+ *   and each entry is rounded as q = fl32(h * r) on the E4M3 grid or the
+ *   integer lattice.
  * Entry k uses the threshold of global index entry_base + k.
  * Returns 0, or -1 on bad arguments.
  */
@@ -385,8 +454,8 @@ int orc_requantize(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step
                    uint64_t entry_base, uint64_t block, int64_t n, int64_t group, const float *h,
                    void *codes, float *scale) {
     ensure_init();
-    if (f < 0 || f > 3 || n < 0 || block == 0) return -1;
-    if (f != ORC_E4M3) {
+    if (f < 0 || f >= ORC_NFMT || n < 0 || block == 0) return -1;
+    if (!is_scaled(f)) {
         for (int64_t k = 0; k < n; ++k) {
             uint32_t U = threshold24(rule, seed, layer, step, entry_base + (uint64_t)k, block);
             store_code(f, codes, k, orc_round(f, rule, h[k], U));
@@ -400,13 +469,18 @@ int orc_requantize(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step
             float a = fabsf(h[k]);
             if (a > m) m = a;
         }
-        float s = m / 448.0f;
+        const float qmax = (f == ORC_E4M3) ? 448.0f : (float)int_qmax(f);
+        float s = m / qmax;
         if (!(s >= FLT_MIN)) s = 0.0f;
         scale[g0 / group] = s;
         float r = (s == 0.0f) ? 0.0f : 1.0f / s;
         for (int64_t k = g0; k < g0 + group; ++k) {
             uint32_t c;
-            if (isnan(h[k])) {
+            if (is_int(f)) {
+                const uint32_t U =
+                    threshold24(rule, seed, layer, step, entry_base + (uint64_t)k, block);
+                c = (s == 0.0f) ? 0u : int_code(f, round_to_int(int_qmax(f), rule, h[k] * r, U));
+            } else if (isnan(h[k])) {
                 c = signbit(h[k]) ? GRID[ORC_E4M3].neg_nan : GRID[ORC_E4M3].pos_nan;
             } else if (s == 0.0f) {
                 c = signbit(h[k]) ? GRID[ORC_E4M3].neg_zero : GRID[ORC_E4M3].pos_zero;
@@ -427,7 +501,8 @@ int orc_requantize(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step
  *
  * Layout (row-major, contiguous):
  *   state  [batch][nheads][headdim][dstate] codes, updated in place
- *   scale  E4M3 only: one fp32 per group of entries (group 0 = one head)
+ *   scale  E4M3, INT8, INT4: one fp32 per group of entries (group 0 = one head)
+ *          INT4 state rows hold dstate / 2 bytes (dstate even)
  *   x      [batch][nheads][headdim]        dt [batch][nheads]
  *   A      [nheads] (a_per_state = 0, Mamba-2) or [nheads][dstate] (= 1, Mamba-1)
  *   B, C   [batch][ngroups][dstate]; head h uses group h / (nheads / ngroups)
@@ -446,12 +521,13 @@ int orc_state_update(int f, int rule, uint32_t seed, uint32_t layer, uint32_t st
                      const float *A, const float *B, const float *C, const float *D, double *y,
                      float *hnew) {
     ensure_init();
-    if (f < 0 || f > 3 || batch < 0 || nheads <= 0 || headdim <= 0 || dstate <= 0 ||
+    if (f < 0 || f >= ORC_NFMT || batch < 0 || nheads <= 0 || headdim <= 0 || dstate <= 0 ||
         ngroups <= 0 || nheads % ngroups != 0 || block == 0)
         return -1;
     const int64_t head_size = headdim * dstate;
     const int64_t n_total = batch * nheads * head_size;
-    if (f == ORC_E4M3) {
+    if (f == ORC_INT4 && dstate % 2 != 0) return -1;
+    if (is_scaled(f)) {
         if (group == 0) group = head_size;
         if (group < 0 || n_total % group != 0) return -1;
     }
@@ -477,7 +553,7 @@ int orc_state_update(int f, int rule, uint32_t seed, uint32_t layer, uint32_t st
                     const float v = code_value(f, load_code(f, state, k));
                     const float w = dx * Bg[n];
                     float h_new;
-                    if (f == ORC_E4M3) {
+                    if (is_scaled(f)) {
                         const float dAs = dA * scale[k / group]; /* decay times old scale */
                         h_new = fmaf(dAs, v, w);
                     } else {

@@ -1,0 +1,162 @@
+"""Pins of the oracle's INT8 / INT4 block-scaled formats (CPU only).
+
+Definitions (Section 2 "Low-precision storage"; Appendix B "Formats"): INTb is
+symmetric, qmax = 2^(b-1) - 1, block scale s = max|h| / qmax kept in fp32, values
+clamped to [-qmax, qmax]; rounding is eq. (dither) with step s. Expected values
+come from exact rational arithmetic (fractions), numpy's round-half-to-even, the
+two's complement definition of the codes and an independent float64 evaluation
+of the recurrence.
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from paper_2609_39185_amd import workloads as wl
+
+TWO24 = 1 << 24
+QMAX = {"int8": 127, "int4": 7}
+
+
+def _signed(fmt, codes):
+    c = np.asarray(codes).astype(np.int64)
+    return np.where(c >= (128 if fmt == "int8" else 8), c - (256 if fmt == "int8" else 16), c)
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4"])
+def test_value_set_is_the_symmetric_lattice(orc, fmt):
+    vals, codes = orc.grid(fmt)
+    q = QMAX[fmt]
+    assert np.array_equal(vals, np.arange(-q, q + 1))
+    # two's complement codes, no code for -2^(b-1)
+    assert np.array_equal(_signed(fmt, codes), np.arange(-q, q + 1))
+    assert orc.code_rank(fmt, [0x80 if fmt == "int8" else 0x8])[0] == -1
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4"])
+def test_dither_rule_is_eq_dither_exactly(orc, fmt):
+    """floor(q + U/2^24) in exact rationals, clamped to [-qmax, qmax]."""
+    rng = np.random.default_rng(17)
+    q = QMAX[fmt]
+    n = 4000
+    x = (rng.uniform(-1.3, 1.3, n) * q * np.exp(rng.uniform(-12, 0, n))).astype(np.float32)
+    x[:40] = np.float32(0.5) + np.arange(40, dtype=np.float32)  # lattice midpoints
+    x[40:60] = np.arange(-10, 10, dtype=np.float32)              # lattice points
+    U = rng.integers(0, TWO24, n).astype(np.uint32)
+    U[:8] = [0, TWO24 - 1, 1, TWO24 - 2, 1 << 23, (1 << 23) - 1, (1 << 23) + 1, 3]
+    got = _signed(fmt, orc.round_values(fmt, "weyl", x, U))
+    for xi, ui, gi in zip(x, U, got):
+        k = int(np.floor(Fraction(float(xi)) + Fraction(int(ui), TWO24)))
+        assert gi == max(-q, min(q, k)), (xi, ui, gi)
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4"])
+def test_rtn_is_round_half_even(orc, fmt):
+    rng = np.random.default_rng(4)
+    q = QMAX[fmt]
+    x = (rng.uniform(-1.2, 1.2, 20000) * q).astype(np.float32)
+    x[:30] = np.arange(-15, 15, dtype=np.float32) + np.float32(0.5)   # exact ties
+    got = _signed(fmt, orc.round_values(fmt, "rtn", x))
+    want = np.clip(np.rint(x.astype(np.float64)), -q, q).astype(np.int64)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4"])
+def test_nan_is_stored_as_zero(orc, fmt):
+    for rule in ("rtn", "sr", "weyl"):
+        assert orc.round_values(fmt, rule, [np.nan], [123])[0] == 0
+
+
+def test_int4_packs_two_entries_per_byte(orc):
+    """Entry 2j sits in the low nibble of byte j, entry 2j+1 in the high nibble."""
+    h = np.array([1, -1, 7, -7, 0, 3, -4, 2], np.float32)
+    codes, scale = orc.requantize("int4", "rtn", h, group=8)
+    assert scale[0] == np.float32(1.0)
+    assert list(codes) == [0xF1, 0x97, 0x30, 0x2C]
+    assert np.array_equal(orc.dequantize("int4", codes, scale, 8), h)
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4"])
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+def test_requantize_block_scale(orc, fmt, rule):
+    """s = fl32(max|h| / qmax) per block; codes round q = fl32(h fl32(1/s)) by the rule;
+    every value lands within one step (half a step for RTN) of h."""
+    rng = np.random.default_rng(8)
+    group, nb = 16, 300
+    q = QMAX[fmt]
+    h = (rng.standard_normal(group * nb) * np.exp(rng.uniform(-6, 3, group * nb))).astype(np.float32)
+    h[:group] = 0.0
+    h[group:2 * group] *= np.float32(1e-40)   # scale below the smallest normal: stored as 0
+    codes, scale = orc.requantize(fmt, rule, h, group=group, step=5, layer=2, block=16)
+    hg = h.reshape(nb, group)
+    s = (np.abs(hg).max(axis=1) / np.float32(q)).astype(np.float32)
+    s[s < np.finfo(np.float32).tiny] = 0.0
+    assert np.array_equal(scale, s)
+    k = _signed(fmt, orc.entry_codes(fmt, codes)).reshape(nb, group)
+    assert np.all(k[:2] == 0)
+    live = s > 0
+    r = (np.float32(1.0) / s[live]).astype(np.float32)
+    qv = (hg[live] * r[:, None]).astype(np.float32).astype(np.float64)
+    U = orc.thresholds(rule, 0, 2, 5, 0, group * nb, 16).reshape(nb, group)[live]
+    if rule == "rtn":
+        want = np.clip(np.rint(qv), -q, q)
+    else:
+        want = np.clip(np.floor(qv + U / TWO24), -q, q)
+    assert np.array_equal(k[live], want)
+    deq = orc.dequantize(fmt, codes, scale, group).reshape(nb, group)
+    tol = (0.5 if rule == "rtn" else 1.0) * s[live, None] * (1 + 1e-5)
+    assert np.all(np.abs(deq[live] - hg[live]) <= tol)
+    assert np.all(np.abs(hg[~live]) <= q * np.finfo(np.float32).tiny)  # flushed blocks
+
+
+@pytest.mark.parametrize("rule", ["sr", "weyl"])
+def test_int_dithers_are_unbiased(orc, rule):
+    """Averaged over many steps the dithered INT4 value of a fixed h converges to h."""
+    rng = np.random.default_rng(21)
+    group = 16
+    h = rng.uniform(-1, 1, group).astype(np.float32)
+    h[0] = 1.0  # the block maximum: s = 1/7
+    T = 2048
+    acc = np.zeros(group)
+    for t in range(T):
+        c, s = orc.requantize("int4", rule, h, group=group, step=t, block=16)
+        acc += orc.dequantize("int4", c, s, group)
+    step = 1.0 / 7
+    bias = (acc / T - h) / step
+    tol = 4 * 0.5 / np.sqrt(T) if rule == "sr" else 0.01
+    assert np.all(np.abs(bias) < tol)
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4"])
+def test_int_step_is_the_recurrence_with_block_scale(orc, fmt):
+    """h_new = fma(fl32(dA s_old), k, w) against a float64 evaluation of eq. (rec);
+    y from the pre-rounding state; the new scale is max|h_new| / qmax per block."""
+    batch, nheads, headdim, dstate, ngroups, group = 2, 4, 8, 32, 2, 16
+    A, D = wl.layer_params("mamba2", nheads, dstate, 7)
+    x, dt, B, C = wl.step_inputs(batch, nheads, headdim, dstate, ngroups, 7)
+    p = {k: v.numpy() for k, v in dict(A=A, D=D, x=x, dt=dt, B=B, C=C).items()}
+    rng = np.random.default_rng(2)
+    h0 = (rng.standard_normal((batch, nheads, headdim, dstate)) * 0.1).astype(np.float32)
+    codes0, s0 = orc.requantize(fmt, "rtn", h0, group=group)
+    per = 2 if fmt == "int4" else 1
+    codes0 = codes0.reshape(batch, nheads, headdim, dstate // per)
+    new, s1, y, hnew = orc.state_update(fmt, "weyl", codes0, s0, p["x"], p["dt"], p["A"], p["B"],
+                                        p["C"], p["D"], group=group, block=32)
+    prev = orc.dequantize(fmt, codes0, s0, group).astype(np.float64).reshape(h0.shape)
+    hpg = nheads // ngroups
+    Bh = np.repeat(p["B"].astype(np.float64), hpg, axis=1)
+    Ch = np.repeat(p["C"].astype(np.float64), hpg, axis=1)
+    dtv = p["dt"].astype(np.float64)
+    dA = np.exp(dtv * p["A"].astype(np.float64)[None, :])[:, :, None, None]
+    w = (dtv[:, :, None] * p["x"].astype(np.float64))[..., None] * Bh[:, :, None, :]
+    ref = dA * prev + w
+    tol = 4e-7 * (np.abs(dA * prev) + np.abs(w)) + 1e-30
+    assert np.all(np.abs(hnew - ref) <= tol)
+    yref = ((Ch[:, :, None, :] * hnew.astype(np.float64)).sum(-1)
+            + p["D"].astype(np.float64)[None, :, None] * p["x"].astype(np.float64))
+    assert np.allclose(y, yref, rtol=1e-12, atol=1e-12)
+    m = np.abs(hnew.reshape(-1, group)).max(axis=1).astype(np.float32)
+    assert np.array_equal(s1, (m / np.float32(QMAX[fmt])).astype(np.float32))
+    # and the codes are the requantization of hnew
+    want, _ = orc.requantize(fmt, "weyl", hnew, group=group, block=32)
+    assert np.array_equal(new.ravel(), want)
