@@ -33,9 +33,14 @@ METRIC = "quantized state-update HBM GB/s (state R+W) & % of peak; decode steps/
 def parse_args():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 20; with --state-error the workload's steps)")
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="hybrid_m2_stack")
+    ap.add_argument("--workload", default=None,
+                    help="default hybrid_m2_stack (m1_long with --state-error)")
+    ap.add_argument("--state-error", action="store_true",
+                    help="instead of throughput: quantized states vs an FP32 twin in lockstep")
+    ap.add_argument("--block", type=int, default=512, help="--state-error: steps per reported block")
     ap.add_argument("--variants", default="bf16:weyl,bf16:sr,bf16:rtn,e4m3:weyl,e4m3:sr,e4m3:rtn",
                     help="comma-separated format:rule list; the first is the headline")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
@@ -55,6 +60,8 @@ def state_bytes_per_entry(fmt: str) -> float:
 
 def main() -> int:
     args = parse_args()
+    if args.workload is None:
+        args.workload = "m1_long" if args.state_error else "hybrid_m2_stack"
     if args.summarize_profiles:
         return summarize_profiles(args.workload, *args.summarize_profiles)
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -71,6 +78,13 @@ def main() -> int:
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = wl.WORKLOADS[args.workload]
+    if args.state_error:
+        res = state_error_study(w, steps=args.steps or w.steps, layers=args.layers or w.layers,
+                                block=args.block, device=dev)
+        print(json.dumps(res), flush=True)
+        return 0
+    if args.steps is None:
+        args.steps = 20
     L = args.layers or w.layers
     b, H, P, N, G = w.batch, w.nheads, w.headdim, w.dstate, w.ngroups
     n_entries = w.entries_per_layer
@@ -209,6 +223,148 @@ def main() -> int:
     }
     print(json.dumps(line), flush=True)
     return 0
+
+
+SE_RULES = (("rtn", 0), ("sr", 0), ("sr", 1), ("weyl", 0))  # (rule, seed sigma)
+TAU_EDGES = (10.0, 100.0, 1000.0)  # memory bins: tau < 10, 10-100, 100-1000, >= 1000 steps
+
+
+def mean_step_size() -> float:
+    """E[softplus(z - 4)], z ~ N(0, 1): the mean of the synthetic step sizes."""
+    import numpy as np
+
+    z = np.linspace(-12.0, 12.0, 240001)
+    pdf = np.exp(-0.5 * z * z) / np.sqrt(2.0 * np.pi)
+    return float(np.trapezoid(np.logaddexp(0.0, z - 4.0) * pdf, z))
+
+
+def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: str = "fp16",
+                      rules=SE_RULES, on_step=None, init=None) -> dict:
+    """Quantized states against an unrounded FP32 twin, decoded in lockstep on the
+    same teacher-forced inputs (Appendix B, "Open-loop replay" and "Decode regime").
+
+    Every (layer, step) runs the fused update once per rule and once in the FP32
+    format (the twin). Both start from the same stored state. Per block of `block`
+    steps and per layer the error is sum((h_hat - h)^2) / sum(h^2) over entries,
+    batch and steps; the model-level figure is the mean over layers. Errors are also
+    split into memory bins by tau = 1 / (1 - exp(A * E[dt])).
+
+    Inputs: A, D per layer as in the throughput bench; x, dt, B, C for all layers of
+    step t from one generator seeded with splitmix64(4000, t). on_step(t, x, dt, B, C)
+    is called with each step's inputs, and init = {"A", "D", "codes0"} replaces the
+    generated layer parameters and initial codes (both for cross-checks on small sizes).
+    """
+    import numpy as np
+    import torch
+
+    import paper_2609_39185_amd as ssmq
+    from paper_2609_39185_amd import workloads as wl
+
+    if w.family != "mamba1":
+        raise ValueError("the state-error study is defined on the Mamba-1 shapes")
+    b, d, N = w.batch, w.nheads, w.dstate
+    L = layers
+    n_blocks = (steps + block - 1) // block
+    code_dt = wl.CODE_TORCH_DTYPE[fmt]
+    val_dt = {"fp16": torch.float16, "bf16": torch.bfloat16}[fmt]
+    A, D = [], []
+    for ell in range(L):
+        if init is not None:
+            a, dd = init["A"][ell].to(device), init["D"][ell].to(device)
+        else:
+            a, dd = wl.layer_params(w.family, d, N, seed=1000 + ell, device=device)
+        A.append(a.contiguous())
+        D.append(dd.contiguous())
+    codes = {r: torch.empty((L, b, d, 1, N), dtype=code_dt, device=device) for r in rules}
+    twin = torch.empty((L, b, d, 1, N), dtype=torch.float32, device=device)
+    for ell in range(L):
+        if init is not None:
+            c0 = init["codes0"][ell].to(device)
+        else:
+            c0, _ = wl.initial_state(fmt, b, d, 1, N, seed=3000 + ell, device=device)
+        for r in rules:
+            codes[r][ell].copy_(c0)
+        twin[ell].copy_(c0.view(val_dt).float())
+    twin_codes = twin.view(torch.int32)
+    y = torch.empty((b, d, 1), dtype=torch.float32, device=device)
+
+    # memory bins of each (layer, channel, n)
+    dt_mean = mean_step_size()
+    abar = torch.exp(torch.stack(A) * dt_mean)                       # [L, d, N]
+    tau = 1.0 / (1.0 - abar)
+    bins = torch.bucketize(tau, torch.tensor(TAU_EDGES, device=device))  # [L, d, N] in 0..3
+    n_bins = len(TAU_EDGES) + 1
+    onehot = torch.nn.functional.one_hot(bins, n_bins).to(torch.float64)  # [L, d, N, n_bins]
+
+    num = {r: torch.zeros((n_blocks, L, n_bins), dtype=torch.float64, device=device) for r in rules}
+    den = torch.zeros((n_blocks, L, n_bins), dtype=torch.float64, device=device)
+    # per-entry sums over batch and the steps of the current block
+    acc = {r: torch.zeros((L, d, N), dtype=torch.float64, device=device) for r in rules}
+    acc_h = torch.zeros((L, d, N), dtype=torch.float64, device=device)
+    stream = torch.cuda.current_stream(device)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for t in range(1, steps + 1):
+        g = torch.Generator(device=device)
+        g.manual_seed(wl.splitmix64(4000, t))
+        x = torch.randn((L, b, d, 1), generator=g, device=device)
+        dt = torch.nn.functional.softplus(torch.randn((L, b, d), generator=g, device=device) - 4.0)
+        B = torch.randn((L, b, 1, N), generator=g, device=device)
+        C = torch.randn((L, b, 1, N), generator=g, device=device)
+        if on_step is not None:
+            on_step(t, x, dt, B, C)
+        for ell in range(L):
+            args = (x[ell], dt[ell], A[ell], B[ell], C[ell], D[ell], y)
+            ssmq.state_update(twin_codes[ell], None, *args, rule="rtn", fmt="fp32",
+                              dither_block=w.dither_block, layer=ell, step=t, stream=stream)
+            for r in rules:
+                ssmq.state_update(codes[r][ell], None, *args, rule=r[0], fmt=fmt, seed=r[1],
+                                  dither_block=w.dither_block, layer=ell, step=t, stream=stream)
+        acc_h += twin.square().sum(dim=(1, 3))
+        for r in rules:
+            e = codes[r].view(val_dt).float().sub_(twin)
+            acc[r] += e.square_().sum(dim=(1, 3))
+        if t % block == 0 or t == steps:
+            k = (t - 1) // block
+            den[k] = torch.einsum("ldn,ldnk->lk", acc_h, onehot)
+            acc_h.zero_()
+            for r in rules:
+                num[r][k] = torch.einsum("ldn,ldnk->lk", acc[r], onehot)
+                acc[r].zero_()
+            print(f"state-error study: {t} of {steps} steps, "
+                  f"{time.perf_counter() - t_start:.1f} s", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+
+    def name(r):
+        return r[0] if r[0] != "sr" else f"sr_seed{r[1]}"
+
+    out_rules, out_bins = {}, {}
+    for r in rules:
+        tot = num[r].sum(-1) / den.sum(-1)                                   # [blocks, L]
+        out_rules[name(r)] = [float(v) for v in tot.mean(-1)]
+        per_bin = num[r] / den                                               # [blocks, L, bins]
+        out_bins[name(r)] = {}
+        for j in range(n_bins):
+            if float(den[..., j].sum()) > 0:
+                lab = ("<10", "10-100", "100-1000", ">=1000")[j]
+                out_bins[name(r)][lab] = [float(v) for v in per_bin[..., j].nanmean(-1)]
+    ref = name(("sr", 0))
+    share = [float(v) for v in torch.bincount(bins.flatten(), minlength=n_bins).double() / bins.numel()]
+    return {
+        "study": "state_error",
+        "metric": "relative state error sum((h_hat-h)^2)/sum(h^2) per block, mean over layers",
+        "workload": w.name, "format": fmt, "batch": b, "d_inner": d, "dstate": N, "layers": L,
+        "steps": steps, "block": block, "dither_block": w.dither_block, "data": "synthetic",
+        "mean_dt": dt_mean, "tau_bin_share": dict(zip(("<10", "10-100", "100-1000", ">=1000"), share)),
+        "error": out_rules,
+        "error_over_sr_seed0": {k: [a / c for a, c in zip(v, out_rules[ref])]
+                                for k, v in out_rules.items()},
+        "error_by_tau_bin": out_bins,
+        "wall_s": elapsed,
+        "ms_per_step": 1e3 * elapsed / steps,
+        "launches_per_step": L * (1 + len(rules)),
+    }
 
 
 def kernel_sources_digest() -> str:
