@@ -41,7 +41,8 @@ def parse_args():
     ap.add_argument("--state-error", action="store_true",
                     help="instead of throughput: quantized states vs an FP32 twin in lockstep")
     ap.add_argument("--block", type=int, default=512, help="--state-error: steps per reported block")
-    ap.add_argument("--variants", default="bf16:weyl,bf16:sr,bf16:rtn,e4m3:weyl,e4m3:sr,e4m3:rtn",
+    ap.add_argument("--variants", default="bf16:weyl,bf16:sr,bf16:rtn,e4m3:weyl,e4m3:sr,e4m3:rtn,"
+                                          "int8:weyl,int8:sr,int8:rtn,int4:weyl,int4:sr,int4:rtn",
                     help="comma-separated format:rule list; the first is the headline")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -55,7 +56,19 @@ def parse_args():
 
 
 def state_bytes_per_entry(fmt: str) -> float:
-    return {"bf16": 2, "fp16": 2, "e4m3": 1, "fp32": 4}[fmt]
+    return {"bf16": 2, "fp16": 2, "e4m3": 1, "fp32": 4, "int8": 1, "int4": 0.5}[fmt]
+
+
+def state_bytes_per_launch(w, fmt: str) -> int:
+    """Algorithmic bytes of one layer's update: codes read and written, plus each
+    group scale read and written (4 B each way)."""
+    from paper_2609_39185_amd import workloads as wl
+
+    n = w.entries_per_layer
+    total = int(n * state_bytes_per_entry(fmt) * 2)
+    if fmt in ("e4m3", "int8", "int4"):
+        total += (n // (wl.scale_group_of(w, fmt) or w.headdim * w.dstate)) * 8
+    return total
 
 
 def main() -> int:
@@ -99,8 +112,8 @@ def main() -> int:
         y = torch.empty((b, H, P), dtype=torch.float32, device=dev)
         states = {}
         for f in fmts:
-            states[f] = wl.initial_state(f, b, H, P, N, seed=3000 + ell, group=w.scale_group,
-                                         device=dev)
+            states[f] = wl.initial_state(f, b, H, P, N, seed=3000 + ell,
+                                         group=wl.scale_group_of(w, f), device=dev)
         layers.append(dict(A=A, D=D, x=x, dt=dt, B=B, C=C, y=y, states=states))
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream(dev)
@@ -112,7 +125,7 @@ def main() -> int:
                 events[ell][0].record(stream)
             ssmq.state_update(st, sc, lay["x"], lay["dt"], lay["A"], lay["B"], lay["C"], lay["D"],
                               lay["y"], rule=rule, fmt=fmt, dither_block=w.dither_block,
-                              scale_group=w.scale_group, layer=ell, step=t, seed=0,
+                              scale_group=wl.scale_group_of(w, fmt), layer=ell, step=t, seed=0,
                               stream=stream)
             if events is not None:
                 events[ell][1].record(stream)
@@ -137,9 +150,7 @@ def main() -> int:
         total_ms = start.elapsed_time(stop)
         launch_ms = [e[0].elapsed_time(e[1]) for step_ev in ev for e in step_ev]
         ms_step = total_ms / args.steps
-        sbytes = n_entries * state_bytes_per_entry(fmt) * 2
-        if fmt == "e4m3":
-            sbytes += (n_entries // (w.scale_group or P * N)) * 8
+        sbytes = state_bytes_per_launch(w, fmt)
         avg_launch_ms = sum(launch_ms) / len(launch_ms)
         results[f"{fmt}:{rule}"] = {
             "ms_per_step": ms_step,
@@ -213,7 +224,8 @@ def main() -> int:
         "config": {"workload": w.name, "family": w.family, "batch": b, "layers": L, "nheads": H,
                    "headdim": P, "dstate": N, "ngroups": G, "format": head_fmt,
                    "rule": head_rule, "dither_block": w.dither_block,
-                   "scale_group": w.scale_group or P * N},
+                   "scale_group": (wl.scale_group_of(w, head_fmt) or P * N)
+                   if head_fmt in ("e4m3", "int8", "int4") else None},
         "pct_of_peak": head["pct_of_peak"],
         "steps_per_s": head["steps_per_s"],
         "roofline": roof,
@@ -396,7 +408,7 @@ def load_traffic(workload: str):
 
 
 # rocprofv3 names the update kernels k_update_slab<F, R, NT, CPT> with these codes
-_FMT_CODE = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3}
+_FMT_CODE = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3, "int8": 4, "int4": 5}
 _RULE_CODE = {"rtn": 0, "sr": 1, "weyl": 2}
 
 
@@ -464,9 +476,7 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
         if key is None:
             continue
         fmt = key.split(":")[0]
-        algo = n_entries * state_bytes_per_entry(fmt) * 2
-        if fmt == "e4m3":
-            algo += (n_entries // (w.scale_group or w.headdim * w.dstate)) * 8
+        algo = state_bytes_per_launch(w, fmt)
         fk = statistics.mean(v)
         wk = statistics.mean(write.get((k, g), [float("nan")]))
         traffic = fk * 1024.0 * f_fetch + wk * 1024.0 * f_write
@@ -546,7 +556,8 @@ def cpu_baseline(w, variant, target_s):
     P, N = w.headdim, w.dstate
     A, D = wl.layer_params(w.family, w.nheads, N, seed=1000)
     x, dt, B, C = wl.step_inputs(1, w.nheads, P, N, w.ngroups, seed=2000)
-    codes, scale = wl.initial_state(fmt, 1, w.nheads, P, N, seed=3000, group=w.scale_group)
+    codes, scale = wl.initial_state(fmt, 1, w.nheads, P, N, seed=3000,
+                                    group=wl.scale_group_of(w, fmt))
     codes_np = wl.to_numpy_codes(fmt, codes)
     args = (None if scale is None else scale.numpy(), x.numpy(), dt.numpy(), A.numpy(),
             B.numpy(), C.numpy(), D.numpy())
@@ -557,7 +568,7 @@ def cpu_baseline(w, variant, target_s):
         t0 = time.perf_counter()
         oracle.state_update(fmt, rule, c, sc, args[1][:, :nh], args[2][:, :nh], args[3][:nh],
                             args[4][:, :1], args[5][:, :1], args[6][:nh], block=w.dither_block,
-                            group=w.scale_group, step=1)
+                            group=wl.scale_group_of(w, fmt), step=1)
         return time.perf_counter() - t0
 
     probe_heads = w.nheads // w.ngroups   # the heads of one B/C group

@@ -54,7 +54,12 @@ typedef enum {
     SSMQ_BF16 = 1,      /* bfloat16 codes, no scale                                      */
     SSMQ_FP8_E4M3 = 2,  /* OCP E4M3FN codes with one fp32 scale per group, max 448,
                            saturating                                                    */
-    SSMQ_FP32 = 3       /* unrounded fp32 (a full-precision twin); the rule is ignored   */
+    SSMQ_FP32 = 3,      /* unrounded fp32 (a full-precision twin); the rule is ignored   */
+    SSMQ_INT8 = 4,      /* symmetric INT8, one fp32 block scale per group, codes
+                           -127..127 two's complement, one byte per entry              */
+    SSMQ_INT4 = 5       /* symmetric INT4, one fp32 block scale per group, codes -7..7
+                           two's complement, two entries per byte (even entry in the
+                           low nibble)                                                 */
 } ssmq_format;
 
 /* Shape of one layer's state cache [batch][nheads][headdim][dstate]. */
@@ -75,8 +80,9 @@ typedef struct {
                               c = i % dither_block of the flat entry index i; a power of
                               two. 16 for Mamba models, the state dimension for hybrids
                               (Section 2 "Low-precision storage")                           */
-    int32_t scale_group;   /* E4M3: entries per fp32 scale, a power of two >= 16 that
-                              divides headdim*dstate; 0 = one scale per head               */
+    int32_t scale_group;   /* E4M3, INT8, INT4: entries per fp32 scale, a power of two
+                              >= 16 that divides headdim*dstate; 0 = one scale per head.
+                              The paper's blocks: 16 (Mamba), 128 (hybrids)               */
     uint32_t seed;         /* sigma (Appendix B "Dithers"; SR key)                          */
     uint32_t layer;        /* l (Appendix B "Dithers"; SR key)                              */
     uint32_t step;         /* t, the integer phase counter (Section 5.4, "Computing the
@@ -90,30 +96,34 @@ typedef struct {
  * ssmq_state_update -- one decode step of the selective-state update, in place.
  *
  * Defines (Section 2, eq. (rec); Appendix B "Runners", Mamba-1 and Mamba-2):
- *   h_prev = decode(state)                 (E4M3: code value * old group scale)
+ *   h_prev = decode(state)                 (E4M3, INT8, INT4: code value * old group
+ *                                           scale, taken as dA * h_prev =
+ *                                           fl32(dA * scale) * code value)
  *   dA     = exp(dt * A)                   (per head, or per (head, n) for Mamba-1)
  *   h_new  = dA * h_prev + (dt * x_p) * B_n
  *   y_p    = sum_n C_n * h_new + D * x_p   (from the unrounded h_new)
- *   state  = Q_u(h_new) under (rule, format); E4M3 first sets each group scale to
- *            max|h_new| / 448 and rounds h_new * (1/scale) (Appendix B "Formats").
+ *   state  = Q_u(h_new) under (rule, format); E4M3, INT8 and INT4 first set each
+ *            group scale to max|h_new| / qmax (448, 127, 7) and round
+ *            h_new * (1/scale) on their grid (Appendix B "Formats").
  * Entry i = entry_base + flat index uses threshold u_(i,step) (see ssmq_dither_fill).
  *
  * Arguments (device pointers; alignment in brackets):
- *   state        [batch][nheads][headdim][dstate] codes (2 B fp16/bf16, 1 B E4M3,
- *                4 B fp32), read and overwritten [16 B]
- *   state_scale  E4M3 only: [batch*nheads*headdim*dstate / group] fp32, read (old
- *                scales) and overwritten (new scales) [4 B]; NULL otherwise
+ *   state        [batch][nheads][headdim][dstate] codes (2 B fp16/bf16, 1 B E4M3
+ *                and INT8, 4 B fp32, 1/2 B INT4), read and overwritten [16 B]
+ *   state_scale  E4M3, INT8, INT4: [batch*nheads*headdim*dstate / group] fp32, read
+ *                (old scales) and overwritten (new scales) [4 B]; NULL otherwise
  *   x            [batch][nheads][headdim] fp32 [4 B]
  *   dt           [batch][nheads] fp32, the step size after softplus [4 B]
  *   A            [nheads] [4 B] or [nheads][dstate] [16 B] fp32 (negative decay rates)
  *   B, C         [batch][ngroups][dstate] fp32 [16 B]
  *   D            [nheads] fp32, or NULL for no skip term [4 B]
  *   y            [batch][nheads][headdim] fp32, written [4 B]
- * Requirements: a state row splits into 16-byte chunks (dstate % 8 == 0 for
- * fp16/bf16, % 16 for E4M3, % 4 for fp32) whose count is a power of two <= 64;
- * nheads % ngroups == 0. E4M3 groups are either one head (when headdim*dstate is
- * 4096, 8192, 16384 or 32768 entries and A is per head) or a power of two of at
- * most 1024 entries. Other shapes return SSMQ_EUNSUPPORTED.
+ * Requirements: a state row splits into chunks (dstate % 8 == 0 for fp16/bf16,
+ * % 16 for E4M3, INT8 and INT4, % 4 for fp32) whose count is a power of two
+ * <= 64; nheads % ngroups == 0. Scale groups are either one head (when
+ * headdim*dstate is 4096 to 131072 entries, a power of two, and A is per head)
+ * or a power of two of at most 1024 entries. Other shapes return
+ * SSMQ_EUNSUPPORTED.
  */
 ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void* state,
                               float* state_scale, const float* x, const float* dt,
@@ -124,18 +134,20 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
  * ssmq_requantize -- write fp32 values into a storage format under a rule.
  *
  * The rounding step alone (Section 2, eq. (dither); Appendix B "Formats"):
- * codes[k] = Q_u(h[k]) with the threshold of entry entry_base + k. For E4M3 each
- * group of consecutive entries (q->scale_group, or head_size when that is 0)
- * gets scale[g] = fl32(max|h| / 448), flushed to 0 below 2^-126 (then every
- * code of the group is a signed zero), and codes of fl32(h * fl32(1 / scale))
- * rounded on the E4M3 grid after saturation to +-448. A result of zero keeps
- * the sign of its input; NaN gives the canonical NaN code.
+ * codes[k] = Q_u(h[k]) with the threshold of entry entry_base + k. For E4M3,
+ * INT8 and INT4 each group of consecutive entries (q->scale_group, or head_size
+ * when that is 0) gets scale[g] = fl32(max|h| / qmax) (qmax 448, 127, 7),
+ * flushed to 0 below 2^-126 (then every code of the group is a zero), and codes
+ * of fl32(h * fl32(1 / scale)) rounded on the E4M3 grid or the integer lattice
+ * after saturation to +-qmax. For the float formats a result of zero keeps the
+ * sign of its input and NaN gives the canonical NaN code; the integer formats
+ * store NaN as 0 and round exact ties of RTN to the even integer.
  *
- * Arguments: n_entries >= 0; head_size > 0 (used only for E4M3 with
- * scale_group 0); h [n_entries] fp32 [16 B]; codes [n_entries] codes [16 B];
- * scale E4M3 only [n_entries / group] fp32 (written), else NULL [4 B].
- * E4M3 groups must be multiples of 16 that divide n_entries; entry_base must be
- * a multiple of 16.
+ * Arguments: n_entries >= 0; head_size > 0 (used only for scaled formats with
+ * scale_group 0); h [n_entries] fp32 [16 B]; codes [n_entries] codes (INT4:
+ * n_entries / 2 bytes) [16 B]; scale (E4M3, INT8, INT4) [n_entries / group]
+ * fp32 (written), else NULL [4 B]. Scale groups must be multiples of 16 that
+ * divide n_entries; entry_base must be a multiple of 16.
  */
 ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t head_size,
                             const float* h, void* codes, float* scale, void* stream);

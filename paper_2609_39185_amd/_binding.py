@@ -14,8 +14,11 @@ import torch  # imported first so the HIP runtime is the one torch already loade
 LIBRARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libssmq.so")
 
 RULES = {"rtn": 0, "sr": 1, "weyl": 2}
-FORMATS = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3}
-CODE_BYTES = {"fp16": 2, "bf16": 2, "e4m3": 1, "fp32": 4}
+FORMATS = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3, "int8": 4, "int4": 5}
+CODE_BYTES = {"fp16": 2, "bf16": 2, "e4m3": 1, "fp32": 4, "int8": 1, "int4": 1}
+# entries per element of the code tensor (INT4: two per byte, even entry in the low nibble)
+ENTRIES_PER_CODE = {"fp16": 1, "bf16": 1, "e4m3": 1, "fp32": 1, "int8": 1, "int4": 2}
+SCALED = ("e4m3", "int8", "int4")
 
 _i32, _i64, _u32, _u64, _vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32,
                                ctypes.c_uint64, ctypes.c_void_p)
@@ -101,8 +104,10 @@ def qparams(rule: str, fmt: str, *, dither_block=16, scale_group=0, seed=0, laye
 
 def state_update(state, scale, x, dt, A, B, C, D, y, *, rule: str, fmt: str, dither_block=16,
                  scale_group=0, seed=0, layer=0, step=0, entry_base=0, stream=None) -> None:
-    """ssmq_state_update on [batch, nheads, headdim, dstate] state codes, in place."""
+    """ssmq_state_update on [batch, nheads, headdim, dstate] state codes, in place
+    (INT4: [batch, nheads, headdim, dstate / 2] bytes)."""
     batch, nheads, headdim, dstate = state.shape
+    dstate *= ENTRIES_PER_CODE[fmt]
     if state.element_size() != CODE_BYTES[fmt]:
         raise ValueError(f"state element size {state.element_size()} does not match {fmt}")
     dims = Dims(batch, nheads, headdim, dstate, B.shape[1], 1 if A.dim() == 2 else 0)
@@ -115,8 +120,9 @@ def state_update(state, scale, x, dt, A, B, C, D, y, *, rule: str, fmt: str, dit
 
 def requantize(h, codes, scale, *, rule: str, fmt: str, head_size=0, dither_block=16,
                scale_group=0, seed=0, layer=0, step=0, entry_base=0, stream=None) -> None:
-    """ssmq_requantize: fp32 h -> codes (and E4M3 scales)."""
-    if codes.numel() != h.numel() or codes.element_size() != CODE_BYTES[fmt]:
+    """ssmq_requantize: fp32 h -> codes (and E4M3 / INT8 / INT4 group scales)."""
+    if (codes.numel() * ENTRIES_PER_CODE[fmt] != h.numel()
+            or codes.element_size() != CODE_BYTES[fmt]):
         raise ValueError("codes must match h in size and the format in element size")
     q = qparams(rule, fmt, dither_block=dither_block, scale_group=scale_group, seed=seed,
                 layer=layer, step=step, entry_base=entry_base)

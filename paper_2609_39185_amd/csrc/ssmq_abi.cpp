@@ -36,10 +36,18 @@ int log2i(int64_t v) {
 }
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-int code_bytes(int format) {
-  return format == SSMQ_FP8_E4M3 ? 1 : (format == SSMQ_FP32 ? 4 : 2);
+// Entries per chunk (the unit one lane moves): 16 bytes of fp16/bf16/fp32 or
+// E4M3/INT8 codes, 8 bytes of INT4 codes.
+int chunk_entries(int format) {
+  switch (format) {
+    case SSMQ_FP16: case SSMQ_BF16: return 8;
+    case SSMQ_FP32: return 4;
+    default: return 16;
+  }
 }
-int chunk_entries(int format) { return 16 / code_bytes(format); }
+bool is_scaled(int format) {
+  return format == SSMQ_FP8_E4M3 || format == SSMQ_INT8 || format == SSMQ_INT4;
+}
 
 // Threshold parameters of one call (Appendix B "Dithers"; hash SR) and the
 // offset of entry k within a chunk whose first flat index is a multiple of 16.
@@ -68,7 +76,7 @@ ssmq::Thr make_thr(int rule, uint32_t seed, uint32_t layer, uint32_t step, int32
 ssmq_status check_qparams(const ssmq_qparams* q) {
   if (!q) return fail(SSMQ_EINVAL, "qparams is NULL");
   if (q->rule < SSMQ_RTN || q->rule > SSMQ_WEYL) return fail(SSMQ_EINVAL, "unknown rule %d", q->rule);
-  if (q->format < SSMQ_FP16 || q->format > SSMQ_FP32)
+  if (q->format < SSMQ_FP16 || q->format > SSMQ_INT4)
     return fail(SSMQ_EINVAL, "unknown format %d", q->format);
   if (q->reserved != 0) return fail(SSMQ_EINVAL, "qparams.reserved must be 0");
   if (!is_pow2(q->dither_block) || q->dither_block > (1 << 30))
@@ -121,12 +129,12 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
     return fail(SSMQ_EINVAL, "a_per_state must be 0 or 1");
   if (!state || !x || !dt || !A || !B || !C || !y)
     return fail(SSMQ_EINVAL, "state, x, dt, A, B, C and y must not be NULL");
-  const bool fp8 = q->format == SSMQ_FP8_E4M3;
-  if (fp8 && !state_scale) return fail(SSMQ_EINVAL, "E4M3 needs state_scale");
+  const bool scaled = is_scaled(q->format);  // E4M3, INT8, INT4: one fp32 scale per group
+  if (scaled && !state_scale) return fail(SSMQ_EINVAL, "E4M3, INT8 and INT4 need state_scale");
   if (!aligned(state, 16) || !aligned(B, 16) || !aligned(C, 16) || (d.a_per_state && !aligned(A, 16)))
     return fail(SSMQ_EALIGN, "state, B, C (and A[nheads][dstate]) must be 16-byte aligned");
   if (!aligned(x, 4) || !aligned(dt, 4) || !aligned(A, 4) || !aligned(y, 4) ||
-      (D && !aligned(D, 4)) || (fp8 && !aligned(state_scale, 4)))
+      (D && !aligned(D, 4)) || (scaled && !aligned(state_scale, 4)))
     return fail(SSMQ_EALIGN, "fp32 arrays must be 4-byte aligned");
 
   const int V = chunk_entries(q->format);
@@ -139,7 +147,7 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
       !mul_ok(bh, head_size, &n_total))
     return fail(SSMQ_EINVAL, "state size overflows int64");
   int64_t group = 0;
-  if (fp8) {
+  if (scaled) {
     group = q->scale_group ? q->scale_group : head_size;
     if (group % 16 != 0 || group > head_size || head_size % group != 0)
       return fail(SSMQ_EINVAL, "scale_group %lld must be a multiple of 16 dividing headdim*dstate",
@@ -157,16 +165,16 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
   a.head_size = head_size; a.n_chunks = n_total / V;
   a.entry_base = q->entry_base;
   a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block, a.toff);
-  a.group_shift = fp8 && is_pow2(group) ? log2i(group) : 0;
-  const bool small_groups_ok = !fp8 || (is_pow2(group / 16) && group / 16 <= 64);
+  a.group_shift = scaled && is_pow2(group) ? log2i(group) : 0;
+  const bool small_groups_ok = !scaled || (is_pow2(group / 16) && group / 16 <= 64);
 
   // Slab kernels for per-head A: a workgroup owns whole rows of one head, two
-  // 16-byte chunks per thread; with one E4M3 scale per head the workgroup owns
+  // 16-byte chunks per thread; with one scale per head (scaled formats) the workgroup owns
   // the whole head, four chunks per thread (fewer, fuller threads amortise the
   // per-workgroup scale reduction and its barriers).
   int cfg = -1;
   const int64_t head_chunks = head_size / V;
-  if (d.a_per_state == 0 && fp8 && group == head_size) {
+  if (d.a_per_state == 0 && scaled && group == head_size) {
     switch (head_chunks) {
       case 256: cfg = ssmq::kSlab64x4; break;
       case 512: cfg = ssmq::kSlab128x4; break;
@@ -182,7 +190,7 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
     cfg = (head_chunks % 512 == 0) ? ssmq::kSlab256x2 : ssmq::kSlab256x1;
     a.slabs_per_head = static_cast<int32_t>(
         head_chunks / (ssmq::kSlabThreads[cfg] * ssmq::kSlabChunks[cfg]));
-    a.lanes_per_group = fp8 ? static_cast<int32_t>(group / 16) : 1;
+    a.lanes_per_group = scaled ? static_cast<int32_t>(group / 16) : 1;
   }
   if (cfg >= 0) {  // threshold base advance per pass of NT chunks
     const int64_t step_entries = static_cast<int64_t>(ssmq::kSlabThreads[cfg]) * V;
@@ -202,13 +210,13 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
   if (cfg < 0) {
     if (!small_groups_ok)
       return fail(SSMQ_EUNSUPPORTED,
-                  "E4M3 scale group of %lld entries: supported are powers of two up to 1024 "
+                  "scale group of %lld entries: supported are powers of two up to 1024 "
                   "entries, or one scale per head of 4096 to 131072 entries with A per head",
                   static_cast<long long>(group));
     if ((n_total >> a.dstate_shift) > 0xFFFFFFFFLL || (a.n_chunks + 255) / 256 > 0x7FFFFFFFLL)
       return fail(SSMQ_EUNSUPPORTED, "state too large for one launch");
     cfg = ssmq::kRowKernel;
-    a.lanes_per_group = fp8 ? static_cast<int32_t>(group / 16) : 1;
+    a.lanes_per_group = scaled ? static_cast<int32_t>(group / 16) : 1;
     a.div_headdim = ssmq::make_fastdiv(static_cast<uint32_t>(d.headdim));
   }
   hipError_t e = ssmq::launch_update(a, q->format, q->rule, cfg, d.a_per_state != 0,
@@ -222,27 +230,27 @@ ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t he
   ssmq_status st = check_qparams(q);
   if (st != SSMQ_OK) return st;
   if (n_entries < 0) return fail(SSMQ_EINVAL, "n_entries < 0");
-  const bool fp8 = q->format == SSMQ_FP8_E4M3;
+  const bool scaled = is_scaled(q->format);  // E4M3, INT8, INT4
   int64_t group = 0;
-  if (fp8) {
+  if (scaled) {
     group = q->scale_group ? q->scale_group : head_size;
     if (group <= 0 || group % 16 != 0)
-      return fail(SSMQ_EINVAL, "E4M3 group %lld must be a positive multiple of 16",
+      return fail(SSMQ_EINVAL, "scale group %lld must be a positive multiple of 16",
                   static_cast<long long>(group));
     if (n_entries % group != 0)
-      return fail(SSMQ_EINVAL, "n_entries is not a multiple of the E4M3 group");
+      return fail(SSMQ_EINVAL, "n_entries is not a multiple of the scale group");
   }
   if (n_entries == 0) return ok();
-  if (!h || !codes || (fp8 && !scale)) return fail(SSMQ_EINVAL, "h, codes (and scale) must not be NULL");
-  if (!aligned(h, 16) || !aligned(codes, 16) || (fp8 && !aligned(scale, 4)))
+  if (!h || !codes || (scaled && !scale)) return fail(SSMQ_EINVAL, "h, codes (and scale) must not be NULL");
+  if (!aligned(h, 16) || !aligned(codes, 16) || (scaled && !aligned(scale, 4)))
     return fail(SSMQ_EALIGN, "h and codes must be 16-byte aligned, scale 4-byte aligned");
   ssmq::RequantArgs a{};
   a.h = h; a.codes = codes; a.scale = scale; a.n = n_entries; a.group = group;
   a.entry_base = q->entry_base;
   a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block, a.toff);
   a.lanes_per_group = 64;
-  if (fp8 && group / 16 <= 64 && is_pow2(group / 16)) a.lanes_per_group = static_cast<int32_t>(group / 16);
-  if (!fp8 && (n_entries + 16 * 256 - 1) / (16 * 256) > 0x7FFFFFFFLL)
+  if (scaled && group / 16 <= 64 && is_pow2(group / 16)) a.lanes_per_group = static_cast<int32_t>(group / 16);
+  if (!scaled && (n_entries + 16 * 256 - 1) / (16 * 256) > 0x7FFFFFFFLL)
     return fail(SSMQ_EUNSUPPORTED, "too many entries for one launch");
   hipError_t e = ssmq::launch_requant(a, q->format, q->rule, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));

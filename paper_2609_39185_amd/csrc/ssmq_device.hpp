@@ -20,8 +20,16 @@
 //   bf16  nothing (k = 16 everywhere; NaN and Inf come out canonical);
 //   fp16  the subnormal range |x| < 2^-14 (the conversion is not exact there);
 //   E4M3  NaN (the conversion loses its sign) and |q| < 2^-10, where k > 24.
-// E4M3 values are first clamped to +-448 (saturation); the conversions do not
-// saturate above 464.
+// E4M3 values above 448 (saturation) also take the exact path; the conversions
+// do not saturate above 464.
+//
+// INT8 / INT4 (symmetric, block scale, Appendix B "Formats") round q = h / s
+// on the integer lattice. With q24 = h * (2^24 / s) (exactly q * 2^24 whenever
+// q is a normal float), X = floor(q24) and U the 24-bit threshold,
+// floor(q + U / 2^24) = (X + U) >> 24 exactly: only the top 24 fraction bits of
+// q can decide the comparison with a multiple of 2^-24. The low byte (nibble)
+// of X + U shifted right by 24 is the stored code. Values beyond +-qmax, NaN
+// and |q| < 2^-126 (q24 then differs from q * 2^24) take the exact path.
 //
 // Exact software path. Normal ranges use the carry rule on the magnitude bits.
 // Below the smallest normal of fp16 and E4M3 the grid step is fixed, |x| / step
@@ -36,7 +44,7 @@
 
 namespace ssmq {
 
-enum Fmt : int { kFP16 = 0, kBF16 = 1, kE4M3 = 2, kFP32 = 3 };
+enum Fmt : int { kFP16 = 0, kBF16 = 1, kE4M3 = 2, kFP32 = 3, kINT8 = 4, kINT4 = 5 };
 enum Rule : int { kRTN = 0, kSR = 1, kWEYL = 2 };
 
 // Weyl accumulator (Appendix B "Dithers", hardware form): 2^32 times
@@ -62,11 +70,37 @@ __host__ __device__ inline uint32_t fmix32(uint32_t h) {
   return h;
 }
 
+// A chunk is the unit one lane loads and stores: V entries in CB bytes (16, or
+// 8 for INT4). Scaled formats keep one fp32 scale per group of entries;
+// qmax is the value the group maximum is mapped to.
 template <int F> struct Traits;
-template <> struct Traits<kFP16> { static constexpr int bytes = 2, V = 8; };
-template <> struct Traits<kBF16> { static constexpr int bytes = 2, V = 8; };
-template <> struct Traits<kE4M3> { static constexpr int bytes = 1, V = 16; };
-template <> struct Traits<kFP32> { static constexpr int bytes = 4, V = 4; };
+template <> struct Traits<kFP16> { static constexpr int V = 8, CB = 16; static constexpr bool scaled = false; };
+template <> struct Traits<kBF16> { static constexpr int V = 8, CB = 16; static constexpr bool scaled = false; };
+template <> struct Traits<kFP32> { static constexpr int V = 4, CB = 16; static constexpr bool scaled = false; };
+template <> struct Traits<kE4M3> {
+  static constexpr int V = 16, CB = 16; static constexpr bool scaled = true;
+  static constexpr float qmax = 448.0f;
+};
+template <> struct Traits<kINT8> {
+  static constexpr int V = 16, CB = 16; static constexpr bool scaled = true;
+  static constexpr float qmax = 127.0f;
+};
+template <> struct Traits<kINT4> {
+  static constexpr int V = 16, CB = 8; static constexpr bool scaled = true;
+  static constexpr float qmax = 7.0f;
+};
+template <int F> constexpr bool is_int_fmt = (F == kINT8 || F == kINT4);
+
+template <int CB> struct ChunkOf;
+template <> struct ChunkOf<16> { using type = uint4; };
+template <> struct ChunkOf<8> { using type = uint2; };
+template <int F> using chunk_t = typename ChunkOf<Traits<F>::CB>::type;
+
+// Byte offset of the chunk that starts at entry e (a multiple of V).
+template <int F, typename I>
+__host__ __device__ constexpr I chunk_bytes_at(I e) {
+  return e / static_cast<I>(Traits<F>::V) * static_cast<I>(Traits<F>::CB);
+}
 
 typedef float v2f __attribute__((ext_vector_type(2)));
 typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
@@ -181,12 +215,33 @@ __device__ inline uint32_t round_e4m3(float q, uint32_t thr) {
   return c | sign;
 }
 
+// INT lattice, exact: q = h / s clamped to [-qmax, qmax], then floor(q + u)
+// via the exact fp32 fraction (RTN: nearest, ties to even); NaN -> 0. Returns
+// the two's complement code in the low bits.
+template <bool RTN>
+__device__ inline uint32_t round_int(float q, uint32_t thr, float qmax) {
+  if (q != q) return 0u;
+  q = fminf(fmaxf(q, -qmax), qmax);
+  int k;
+  if constexpr (RTN) {
+    k = static_cast<int>(__builtin_rintf(q));
+  } else {
+    const float I = floorf(q);
+    const float Fr = q - I;  // exact
+    const uint32_t U = thr >> 8;
+    k = static_cast<int>(I) + (Fr >= static_cast<float>(0x1000000u - U) * 0x1p-24f ? 1 : 0);
+  }
+  return static_cast<uint32_t>(k);
+}
+
 template <int F, int R>
 __device__ inline uint32_t round_code(float x, uint32_t thr) {
   constexpr bool rtn = (R == kRTN);
   if constexpr (F == kBF16) return round_bf16<rtn>(x, thr);
   else if constexpr (F == kFP16) return round_fp16<rtn>(x, thr);
   else if constexpr (F == kE4M3) return round_e4m3<rtn>(x, thr);
+  else if constexpr (F == kINT8) return round_int<rtn>(x, thr, 127.0f) & 0xFFu;
+  else if constexpr (F == kINT4) return round_int<rtn>(x, thr, 7.0f) & 0xFu;
   else return __float_as_uint(x);
 }
 
@@ -196,10 +251,10 @@ __device__ inline uint32_t round_code(float x, uint32_t thr) {
 // ---------------------------------------------------------------------------
 template <int F>
 __device__ inline void patch_code(uint32_t (&w)[4], int k, uint32_t c) {
-  if constexpr (Traits<F>::bytes == 4) {
+  constexpr int bits = Traits<F>::CB * 8 / Traits<F>::V;  // code width
+  if constexpr (bits == 32) {
     w[k] = c;
   } else {
-    constexpr int bits = Traits<F>::bytes * 8;
     constexpr int per = 32 / bits;
     const int i = k / per, sh = (k % per) * bits;
     const uint32_t mask = ((1u << bits) - 1u) << sh;
@@ -320,10 +375,115 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// Byte `b` of each of four words, packed little-end first (v_perm_b32).
+template <int B>
+__device__ inline uint32_t pack_bytes(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+  constexpr uint32_t lo = (0x0C0Cu << 16) | ((4u + B) << 8) | B;  // {w0.b, w1.b, 0, 0}
+  const uint32_t p01 = __builtin_amdgcn_perm(w1, w0, lo);
+  const uint32_t p23 = __builtin_amdgcn_perm(w3, w2, lo);
+  return __builtin_amdgcn_perm(p23, p01, 0x05040100u);
+}
+
+// INT8 / INT4 chunk of 16 entries. h: the fp32 values, r = fl32(1 / s) and
+// r24 = 2^24 r of their group (r24 is infinite when 2^24 r overflows).
+// may_saturate: fl32(max|h| r24) > qmax 2^24 (RTN: fl32(max|h| r) > qmax)
+// somewhere in the chunk; maybe_nan: a NaN may be among h.
+template <int F, int R>
+__device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, float r24,
+                                               uint32_t base, const uint32_t* off,
+                                               bool maybe_nan, bool may_saturate) {
+  constexpr float qmax = Traits<F>::qmax;
+  uint32_t S[16];
+  bool rare = maybe_nan || may_saturate;
+  if constexpr (R == kRTN) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) S[k] = static_cast<uint32_t>(static_cast<int>(__builtin_rintf(h[k] * r)));
+  } else {
+    float mn = __builtin_inff();
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float q24 = h[k] * r24;
+      mn = fminf(mn, __builtin_fabsf(q24));
+      S[k] = static_cast<uint32_t>(static_cast<int>(__builtin_floorf(q24))) +
+             (thr_word<R>(base, off[k]) >> 8);
+    }
+    rare = rare || !(mn >= 0x1p-102f);
+  }
+  constexpr int B = (R == kRTN) ? 0 : 3;  // the byte that holds the code
+  uint32_t w[4];
+  if constexpr (F == kINT8) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = pack_bytes<B>(S[4 * i], S[4 * i + 1], S[4 * i + 2], S[4 * i + 3]);
+  } else {
+    // even entries' bytes in one word, odd entries' in another, then nibble-interleave
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int k = 8 * i;
+      const uint32_t ev = pack_bytes<B>(S[k], S[k + 2], S[k + 4], S[k + 6]);
+      const uint32_t od = pack_bytes<B>(S[k + 1], S[k + 3], S[k + 5], S[k + 7]);
+      w[i] = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
+    }
+    w[2] = w[3] = 0u;
+  }
+  if (__builtin_amdgcn_ballot_w64(rare) != 0) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      bool exact;
+      if constexpr (R == kRTN) {
+        exact = !(__builtin_fabsf(h[k] * r) <= qmax);
+      } else {
+        const float a24 = __builtin_fabsf(h[k] * r24);
+        exact = !(a24 >= 0x1p-102f && a24 <= qmax * 0x1p24f);
+      }
+      if (exact) patch_code<F>(w, k, round_code<F, R>(h[k] * r, thr_word<R>(base, off[k])));
+    }
+  }
+  if constexpr (F == kINT8) return make_uint4(w[0], w[1], w[2], w[3]);
+  else return make_uint2(w[0], w[1]);
+}
+
+// Whether some value of a chunk whose largest magnitude is m can exceed qmax
+// once scaled by r (fp32 multiplication is monotone, so the maximum decides).
+// The dithered INT path scales by r24 = 2^24 r and is checked on that product,
+// which also flags an r24 that overflowed.
+template <int F, int R>
+__device__ inline bool saturates(float m, float r) {
+  if constexpr (is_int_fmt<F> && R != kRTN) return m * (r * 0x1p24f) > Traits<F>::qmax * 0x1p24f;
+  else return m * r > Traits<F>::qmax;
+}
+
+// One chunk of fp32 values h -> codes, for every format: r = 1 / s of the
+// chunk's group (ignored by unscaled formats).
+template <int F, int R>
+__device__ inline chunk_t<F> quantize_any(const float (&h)[Traits<F>::V], float r, uint32_t base,
+                                         const uint32_t* off, bool maybe_nan, bool sat) {
+  if constexpr (is_int_fmt<F>) {
+    return quantize_int_chunk<F, R>(h, r, r * 0x1p24f, base, off, maybe_nan, sat);
+  } else if constexpr (F == kE4M3) {
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = h[k] * r;
+    return quantize_chunk<F, R>(v, base, off, maybe_nan, sat);
+  } else {
+    return quantize_chunk<F, R>(h, base, off, maybe_nan, sat);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Decoding code -> its exact value as fp32 (E4M3 without the group scale, via
 // v_cvt_pk_f32_fp8, which decodes OCP E4M3 exactly).
 // ---------------------------------------------------------------------------
+template <int F>
+__device__ inline void decode_chunk(const uint2& raw, float (&out)[Traits<F>::V]) {
+  static_assert(F == kINT4, "8-byte chunks hold INT4 codes");
+  const uint32_t w[2] = {raw.x, raw.y};
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      out[8 * i + j] = static_cast<float>(static_cast<int32_t>(w[i] << (28 - 4 * j)) >> 28);
+}
+
 template <int F>
 __device__ inline void decode_chunk(const uint4& raw, float (&out)[Traits<F>::V]) {
   const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
@@ -343,15 +503,21 @@ __device__ inline void decode_chunk(const uint4& raw, float (&out)[Traits<F>::V]
       out[4 * i + 1] = lo.y;
       out[4 * i + 2] = hi.x;
       out[4 * i + 3] = hi.y;
+    } else if constexpr (F == kINT8) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        out[4 * i + j] = static_cast<float>(static_cast<int8_t>(w[i] >> (8 * j)));
     } else {
       out[i] = __uint_as_float(w[i]);
     }
   }
 }
 
-// E4M3 group scale: s = fl32(m / 448), flushed to zero below 2^-126.
-__device__ inline float e4m3_scale(float m) {
-  const float s = m / 448.0f;
+// Group scale of a scaled format: s = fl32(m / qmax), flushed to zero below
+// 2^-126.
+template <int F>
+__device__ inline float group_scale(float m) {
+  const float s = m / Traits<F>::qmax;
   return (s >= 1.17549435e-38f) ? s : 0.0f;
 }
 
@@ -393,14 +559,27 @@ __device__ inline uint32_t lane_umax(uint32_t v, int width) {
   return v;
 }
 
-// Streaming (nontemporal) 16-byte accesses for the state.
-__device__ inline uint4 load_stream(const void* p) {
+// Streaming (nontemporal) 16- and 8-byte accesses for the state.
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+template <typename C>
+__device__ inline C load_stream(const void* p);
+template <>
+__device__ inline uint4 load_stream<uint4>(const void* p) {
   const v4u v = __builtin_nontemporal_load(static_cast<const v4u*>(p));
   return make_uint4(v.x, v.y, v.z, v.w);
+}
+template <>
+__device__ inline uint2 load_stream<uint2>(const void* p) {
+  const v2u v = __builtin_nontemporal_load(static_cast<const v2u*>(p));
+  return make_uint2(v.x, v.y);
 }
 __device__ inline void store_stream(void* p, const uint4& v) {
   const v4u w = {v.x, v.y, v.z, v.w};
   __builtin_nontemporal_store(w, static_cast<v4u*>(p));
+}
+__device__ inline void store_stream(void* p, const uint2& v) {
+  const v2u w = {v.x, v.y};
+  __builtin_nontemporal_store(w, static_cast<v2u*>(p));
 }
 
 }  // namespace ssmq

@@ -10,7 +10,7 @@
 //   k_update_rows  the same step for any row layout (Mamba-1 with A per (channel,
 //                  n), and Mamba-2 heads smaller than a slab).
 //   k_requant      fp32 -> codes for fp16 / bf16 / fp32, one chunk per thread.
-//   k_requant_e4m3 fp32 -> E4M3 codes with group scales.
+//   k_requant_scaled fp32 -> E4M3 / INT8 / INT4 codes with group scales.
 //   k_dither_fill  the 24-bit thresholds themselves.
 //
 // Layout. A chunk is 16 bytes of codes: V = 8 (fp16, bf16), 16 (E4M3) or 4
@@ -57,18 +57,18 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
   const int r0 = (t >> a.lr_shift) + static_cast<int>(slab) * rows_per_pass * CPT;
   const int64_t tile_base = tile * a.head_size;
   // Uniform bases plus 32-bit lane offsets (a head holds fewer than 2^31 bytes).
-  uint8_t* const hstate = static_cast<uint8_t*>(a.state) + tile_base * Traits<F>::bytes;
+  uint8_t* const hstate = static_cast<uint8_t*>(a.state) + chunk_bytes_at<F>(tile_base);
   const float* const hx = a.x + tile * a.headdim;
   float* const hy = a.y + tile * a.headdim;
   const uint32_t l0 = static_cast<uint32_t>(r0 * a.dstate + n0);  // lane's first entry in the head
   const uint32_t pass = static_cast<uint32_t>(rows_per_pass * a.dstate);  // entries per pass
   const int64_t e0 = tile_base + l0;
 
-  uint4 raw[CPT];
+  chunk_t<F> raw[CPT];
   float xv[CPT];
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    raw[j] = load_stream(hstate + (l0 + j * pass) * Traits<F>::bytes);
+    raw[j] = load_stream<chunk_t<F>>(hstate + chunk_bytes_at<F>(l0 + j * pass));
     xv[j] = hx[r0 + j * rows_per_pass];
   }
   const float dtv = a.dt[tile];
@@ -96,9 +96,10 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
   bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    // E4M3 stores v * s_old; dA * (v * s_old) is evaluated as fma(fl32(dA * s_old), v, w).
+    // Scaled formats store v * s_old; dA * (v * s_old) is evaluated as
+    // fma(fl32(dA * s_old), v, w).
     float dAj = dA;
-    if constexpr (F == kE4M3)
+    if constexpr (Traits<F>::scaled)
       dAj = dA * ((a.lanes_per_group == 0) ? a.scale[tile] : a.scale[(e0 + j * pass) >> a.group_shift]);
     float hp[V];
     decode_chunk<F>(raw[j], hp);
@@ -126,10 +127,10 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
   }
 
   float r[CPT];
-  bool sat[CPT];  // E4M3: fl32(max|h| * r) > 448 somewhere in the chunk
+  bool sat[CPT];  // scaled formats: some |q| of the chunk may exceed qmax
 #pragma unroll
   for (int j = 0; j < CPT; ++j) { r[j] = 1.0f; sat[j] = false; }
-  if constexpr (F == kE4M3) {
+  if constexpr (Traits<F>::scaled) {
     // Lane maxima of |h| ignore NaN and are >= 0, so the cross-lane maximum can
     // compare bit patterns as unsigned integers.
     uint32_t m[CPT];
@@ -152,7 +153,7 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
         uint32_t w = red[0];
 #pragma unroll
         for (int i = 1; i < NW; ++i) w = max(w, red[i]);
-        const float s = e4m3_scale(__uint_as_float(w));
+        const float s = group_scale<F>(__uint_as_float(w));
         if (t == 0) {
           sh[0] = s;
           sh[1] = (s == 0.0f) ? 0.0f : 1.0f / s;
@@ -166,27 +167,24 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
     } else {  // groups of lanes_per_group consecutive lanes of one pass
 #pragma unroll
       for (int j = 0; j < CPT; ++j) {
-        const float s = e4m3_scale(__uint_as_float(lane_umax(m[j], a.lanes_per_group)));
+        const float s = group_scale<F>(__uint_as_float(lane_umax(m[j], a.lanes_per_group)));
         r[j] = (s == 0.0f) ? 0.0f : 1.0f / s;
         if ((t & (a.lanes_per_group - 1)) == 0) a.scale[(e0 + j * pass) >> a.group_shift] = s;
       }
     }
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) sat[j] = __uint_as_float(m[j]) * r[j] > 448.0f;
+    for (int j = 0; j < CPT; ++j) sat[j] = saturates<F, R>(__uint_as_float(m[j]), r[j]);
   }
 
   const uint32_t base0 = thr_base<R>(a.entry_base + static_cast<uint64_t>(e0), a.thr);
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
     const int64_t e = e0 + static_cast<int64_t>(j) * pass;
-    float v[V];
-#pragma unroll
-    for (int k = 0; k < V; ++k) v[k] = (F == kE4M3) ? h[j][k] * r[j] : h[j][k];
     const uint32_t base = (j == 0) ? base0
                           : (a.pass_thr_ok ? base0 + static_cast<uint32_t>(j) * a.pass_thr_inc
                                            : thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr));
-    const uint4 out = quantize_chunk<F, R>(v, base, a.toff, bad[j], sat[j]);
-    store_stream(hstate + (l0 + j * pass) * Traits<F>::bytes, out);
+    const chunk_t<F> out = quantize_any<F, R>(h[j], r[j], base, a.toff, bad[j], sat[j]);
+    store_stream(hstate + chunk_bytes_at<F>(l0 + j * pass), out);
   }
 }
 
@@ -209,7 +207,7 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   const int hh = static_cast<int>(bh - b * static_cast<uint32_t>(a.nheads));
   const int g = static_cast<int>(a.div_hpg.div(static_cast<uint32_t>(hh)));
   uint8_t* const state = static_cast<uint8_t*>(a.state);
-  const uint4 raw = load_stream(state + e * Traits<F>::bytes);
+  const chunk_t<F> raw = load_stream<chunk_t<F>>(state + chunk_bytes_at<F>(e));
   const float xv = a.x[row];
   const float dtv = a.dt[bh];
   const float Dv = a.D ? a.D[hh] : 0.0f;
@@ -226,7 +224,7 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
 #pragma unroll
     for (int k = 0; k < V; ++k) dA[k] = d;
   }
-  if constexpr (F == kE4M3) {  // fold the old group scale into the decay (see k_update_slab)
+  if constexpr (Traits<F>::scaled) {  // fold the old group scale into the decay (see k_update_slab)
     const float s_old = a.scale[e >> a.group_shift];
 #pragma unroll
     for (int k = 0; k < V; ++k) dA[k] = dA[k] * s_old;
@@ -245,19 +243,18 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   ys = lane_sum(ys, a.lanes_per_row);
   if (live && cc == 0) a.y[row] = ys + Dv * xv;
   bool sat = false;
-  if constexpr (F == kE4M3) {
+  float rs = 1.0f;
+  if constexpr (Traits<F>::scaled) {
     float m = 0.0f;
 #pragma unroll
     for (int k = 0; k < V; ++k) m = fmaxf(m, __builtin_fabsf(h[k]));
-    const float s = e4m3_scale(__uint_as_float(lane_umax(__float_as_uint(m), a.lanes_per_group)));
-    const float rs = (s == 0.0f) ? 0.0f : 1.0f / s;
+    const float s = group_scale<F>(__uint_as_float(lane_umax(__float_as_uint(m), a.lanes_per_group)));
+    rs = (s == 0.0f) ? 0.0f : 1.0f / s;
     if (live && (t & (a.lanes_per_group - 1)) == 0) a.scale[e >> a.group_shift] = s;
-#pragma unroll
-    for (int k = 0; k < V; ++k) h[k] *= rs;
-    sat = m * rs > 448.0f;  // rounding is monotone: the chunk maximum decides
+    sat = saturates<F, R>(m, rs);
   }
-  const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff, bad, sat);
-  if (live) store_stream(state + e * Traits<F>::bytes, out);
+  const chunk_t<F> out = quantize_any<F, R>(h, rs, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff, bad, sat);
+  if (live) store_stream(state + chunk_bytes_at<F>(e), out);
 }
 
 // ---------------------------------------------------------------------------
@@ -266,8 +263,9 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
 // ---------------------------------------------------------------------------
 template <int F>
 __device__ inline void store_code(void* codes, int64_t k, uint32_t c) {
-  if constexpr (Traits<F>::bytes == 2) static_cast<uint16_t*>(codes)[k] = static_cast<uint16_t>(c);
-  else if constexpr (Traits<F>::bytes == 4) static_cast<uint32_t*>(codes)[k] = c;
+  constexpr int bytes = Traits<F>::CB / Traits<F>::V;
+  if constexpr (bytes == 2) static_cast<uint16_t*>(codes)[k] = static_cast<uint16_t>(c);
+  else if constexpr (bytes == 4) static_cast<uint32_t*>(codes)[k] = c;
   else static_cast<uint8_t*>(codes)[k] = static_cast<uint8_t>(c);
 }
 
@@ -282,7 +280,7 @@ __global__ __launch_bounds__(256) void k_requant(RequantArgs a) {
     float h[V];
     load_floats<V>(a.h + e, h);
     const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(ge, a.thr), a.toff, chunk_has_nan<V>(h), false);
-    *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + e * Traits<F>::bytes) = out;
+    *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + chunk_bytes_at<F>(e)) = out;
   } else {
     for (int64_t k = e; k < a.n; ++k) {
       const uint64_t gk = a.entry_base + static_cast<uint64_t>(k);
@@ -292,12 +290,13 @@ __global__ __launch_bounds__(256) void k_requant(RequantArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Requantize to E4M3 with group scales. lanes_per_group lanes (a power of two
-// <= 64) work on one group; a wave covers 64 / lanes_per_group groups per
-// iteration and loops over each group's 16-entry chunks.
+// Requantize to a scaled format (E4M3, INT8, INT4) with group scales.
+// lanes_per_group lanes (a power of two <= 64) work on one group; a wave covers
+// 64 / lanes_per_group groups per iteration and loops over each group's
+// 16-entry chunks.
 // ---------------------------------------------------------------------------
-template <int R>
-__global__ __launch_bounds__(256) void k_requant_e4m3(RequantArgs a) {
+template <int F, int R>
+__global__ __launch_bounds__(256) void k_requant_scaled(RequantArgs a) {
   const int lane = threadIdx.x & 63;
   const int LG = a.lanes_per_group;
   const int gpw = 64 / LG;
@@ -319,7 +318,7 @@ __global__ __launch_bounds__(256) void k_requant_e4m3(RequantArgs a) {
         for (int k = 0; k < 16; ++k) m = fmaxf(m, __builtin_fabsf(h[k]));
       }
     }
-    const float s = e4m3_scale(__uint_as_float(lane_umax(__float_as_uint(m), LG)));
+    const float s = group_scale<F>(__uint_as_float(lane_umax(__float_as_uint(m), LG)));
     const float rs = (s == 0.0f) ? 0.0f : 1.0f / s;
     if (live && li == 0) a.scale[grp] = s;
     const int64_t iters = (chunks_per_group + LG - 1) / LG;  // uniform trip count
@@ -331,13 +330,10 @@ __global__ __launch_bounds__(256) void k_requant_e4m3(RequantArgs a) {
       load_floats<16>(a.h + e, h);
       float mc = 0.0f;
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        mc = fmaxf(mc, __builtin_fabsf(h[k]));
-        h[k] *= rs;
-      }
-      const uint4 out = quantize_chunk<kE4M3, R>(h, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff,
-                                                 chunk_has_nan<16>(h), mc * rs > 448.0f);
-      if (ok) *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + e) = out;
+      for (int k = 0; k < 16; ++k) mc = fmaxf(mc, __builtin_fabsf(h[k]));
+      const chunk_t<F> out = quantize_any<F, R>(h, rs, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr),
+                                                a.toff, chunk_has_nan<16>(h), saturates<F, R>(mc, rs));
+      if (ok) *reinterpret_cast<chunk_t<F>*>(static_cast<uint8_t*>(a.codes) + chunk_bytes_at<F>(e)) = out;
     }
   }
 }
@@ -411,6 +407,8 @@ hipError_t launch_update(const UpdateArgs& a, int format, int rule, int cfg, boo
     case kFP16: return launch_update_f<kFP16>(a, rule, cfg, a_per_state, s);
     case kBF16: return launch_update_f<kBF16>(a, rule, cfg, a_per_state, s);
     case kE4M3: return launch_update_f<kE4M3>(a, rule, cfg, a_per_state, s);
+    case kINT8: return launch_update_f<kINT8>(a, rule, cfg, a_per_state, s);
+    case kINT4: return launch_update_f<kINT4>(a, rule, cfg, a_per_state, s);
     default: return launch_update_f<kFP32>(a, rule, cfg, a_per_state, s);
   }
 }
@@ -428,23 +426,28 @@ static hipError_t launch_requant_f(const RequantArgs& a, int rule, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_requant(const RequantArgs& a, int format, int rule, hipStream_t s) {
-  if (format == kE4M3) {
-    const int64_t n_groups = a.n / a.group;
-    const int64_t gpw = 64 / a.lanes_per_group;
-    int64_t blocks = (n_groups + 4 * gpw - 1) / (4 * gpw);
-    if (blocks > 65536) blocks = 65536;
-    const unsigned grid = static_cast<unsigned>(blocks);
-    switch (rule) {
-      case kRTN: hipLaunchKernelGGL((k_requant_e4m3<kRTN>), dim3(grid), dim3(256), 0, s, a); break;
-      case kSR: hipLaunchKernelGGL((k_requant_e4m3<kSR>), dim3(grid), dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL((k_requant_e4m3<kWEYL>), dim3(grid), dim3(256), 0, s, a); break;
-    }
-    return hipGetLastError();
+template <int F>
+static hipError_t launch_requant_scaled(const RequantArgs& a, int rule, hipStream_t s) {
+  const int64_t n_groups = a.n / a.group;
+  const int64_t gpw = 64 / a.lanes_per_group;
+  int64_t blocks = (n_groups + 4 * gpw - 1) / (4 * gpw);
+  if (blocks > 65536) blocks = 65536;
+  const unsigned grid = static_cast<unsigned>(blocks);
+  switch (rule) {
+    case kRTN: hipLaunchKernelGGL((k_requant_scaled<F, kRTN>), dim3(grid), dim3(256), 0, s, a); break;
+    case kSR: hipLaunchKernelGGL((k_requant_scaled<F, kSR>), dim3(grid), dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((k_requant_scaled<F, kWEYL>), dim3(grid), dim3(256), 0, s, a); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_requant(const RequantArgs& a, int format, int rule, hipStream_t s) {
   switch (format) {
     case kFP16: return launch_requant_f<kFP16>(a, rule, s);
     case kBF16: return launch_requant_f<kBF16>(a, rule, s);
+    case kE4M3: return launch_requant_scaled<kE4M3>(a, rule, s);
+    case kINT8: return launch_requant_scaled<kINT8>(a, rule, s);
+    case kINT4: return launch_requant_scaled<kINT4>(a, rule, s);
     default: return launch_requant_f<kFP32>(a, rule, s);
   }
 }

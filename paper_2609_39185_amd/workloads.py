@@ -35,6 +35,7 @@ class Workload:
     rules: tuple = ("rtn", "sr", "weyl")
     dither_block: int = 16
     scale_group: int = 0   # E4M3 entries per scale; 0 = one head
+    int_group: int = 16    # INT8 / INT4 block: 16 (Mamba), the state dimension (hybrids)
     notes: str = ""
     extra: dict = field(default_factory=dict)
 
@@ -62,6 +63,7 @@ WORKLOADS = {
                         notes="long-horizon Mamba-1 shape, batch 16, 64 layers, d_inner 5120"),
     "hybrid_m2_stack": Workload("hybrid_m2_stack", "mamba2", 256, 128, 64, 128, 8, 48, 1024,
                                 ("bf16", "e4m3"), rules=("weyl", "sr", "rtn"), dither_block=128,
+                                int_group=128,
                                 notes="hybrid-style Mamba-2 stack, batch 256, 48 SSM layers, "
                                       "128 heads of 64x128, 8 groups"),
 }
@@ -71,6 +73,13 @@ def _gen(seed: int, device="cpu") -> torch.Generator:
     g = torch.Generator(device=device)
     g.manual_seed(int(seed) & 0x7FFFFFFFFFFFFFFF)
     return g
+
+
+def scale_group_of(w: "Workload", fmt: str) -> int:
+    """Entries per scale of a scaled format on a workload (0 = one head)."""
+    if fmt in ("int8", "int4"):
+        return w.int_group
+    return w.scale_group if fmt == "e4m3" else 0
 
 
 def splitmix64(*words: int) -> int:
@@ -107,17 +116,34 @@ def step_inputs(batch: int, nheads: int, headdim: int, dstate: int, ngroups: int
 
 _TORCH_DTYPE = {"fp16": torch.float16, "bf16": torch.bfloat16, "fp32": torch.float32}
 CODE_TORCH_DTYPE = {"fp16": torch.int16, "bf16": torch.int16, "e4m3": torch.uint8,
-                    "fp32": torch.int32}
+                    "fp32": torch.int32, "int8": torch.uint8, "int4": torch.uint8}
+INT_QMAX = {"int8": 127, "int4": 7}
 
 
 def initial_state(fmt: str, batch: int, nheads: int, headdim: int, dstate: int, seed: int,
                   group: int = 0, device="cpu"):
-    """Stored codes [batch, nheads, headdim, dstate] (and E4M3 group scales).
+    """Stored codes [batch, nheads, headdim, dstate] (and E4M3 / INT group scales).
 
-    Codes are returned as integer tensors (int16 / uint8 / int32 bit patterns).
+    Codes are returned as integer tensors (int16 / uint8 / int32 bit patterns);
+    INT4 packs two entries per byte, [batch, nheads, headdim, dstate / 2].
     """
     g = _gen(splitmix64(seed, 3), device)
     shape = (batch, nheads, headdim, dstate)
+    if fmt in INT_QMAX:
+        # a Gaussian state at the scale's resolution: integers k ~ N(0, (qmax/3)^2)
+        # clamped to +-qmax, scales U[1e-3, 1e-2] per group
+        qmax = INT_QMAX[fmt]
+        head = headdim * dstate
+        group = head if group == 0 else group
+        k = torch.randn(shape, generator=g, device=device, dtype=torch.float32) * (qmax / 3.0)
+        k = k.round_().clamp_(-qmax, qmax).to(torch.int32)
+        u = (k & (0xFF if fmt == "int8" else 0xF)).to(torch.uint8)
+        if fmt == "int4":
+            u = (u[..., 0::2] | (u[..., 1::2] << 4)).to(torch.uint8)
+        n_groups = batch * nheads * head // group
+        scale = (torch.rand((n_groups,), generator=g, device=device, dtype=torch.float32)
+                 * 9e-3 + 1e-3)
+        return u.contiguous(), scale.contiguous()
     if fmt == "e4m3":
         head = headdim * dstate
         group = head if group == 0 else group

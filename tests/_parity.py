@@ -22,8 +22,8 @@ def say(msg: str) -> None:
 
 def code_stats(fmt: str, got: np.ndarray, want: np.ndarray):
     """(number of differing codes, largest distance in storage ulps)."""
-    got = np.asarray(got).ravel()
-    want = np.asarray(want).ravel()
+    got = np.asarray(oracle.entry_codes(fmt, got)).ravel()
+    want = np.asarray(oracle.entry_codes(fmt, want)).ravel()
     idx = np.nonzero(got != want)[0]
     if idx.size == 0:
         return 0, 0
@@ -40,8 +40,9 @@ def code_stats(fmt: str, got: np.ndarray, want: np.ndarray):
 
 def assert_codes(fmt, got, want, what=""):
     n, ulp = code_stats(fmt, got, want)
-    frac = n / max(1, np.asarray(got).size)
-    say(f"  {what}: {n} of {np.asarray(got).size} stored entries differ (max {ulp} ulp)")
+    size = np.asarray(got).size * oracle.entries_per_code_word(fmt)
+    frac = n / max(1, size)
+    say(f"  {what}: {n} of {size} stored entries differ (max {ulp} ulp)")
     assert frac <= MAX_DIFFER_FRACTION and ulp <= MAX_ULP, (what, n, ulp)
 
 
@@ -99,8 +100,8 @@ def check_step(fmt, rule, family, batch, nheads, headdim, dstate, ngroups, seed,
     g_codes, g_scale, g_y = run_update(fmt, rule, codes, scale, x, dt, A, B, C, D, **q)
     r_codes, r_scale, r_y, r_h = oracle_update(fmt, rule, codes, scale, x, dt, A, B, C, D, **q)
     assert_codes(fmt, g_codes, r_codes, what)
-    if fmt == "e4m3":
-        assert np.array_equal(g_scale, r_scale), "E4M3 group scales differ"
+    if fmt in oracle.SCALED:
+        assert np.array_equal(g_scale, r_scale), f"{fmt} group scales differ"
     mag = y_magnitude(C.numpy(), r_h, None if D is None else D.numpy(), x.numpy(),
                       nheads // ngroups)
     assert_y(g_y, r_y, mag, what)
