@@ -41,8 +41,10 @@ def parse_args():
     ap.add_argument("--state-error", action="store_true",
                     help="instead of throughput: quantized states vs an FP32 twin in lockstep")
     ap.add_argument("--block", type=int, default=512, help="--state-error: steps per reported block")
-    ap.add_argument("--variants", default="bf16:weyl,bf16:sr,bf16:rtn,e4m3:weyl,e4m3:sr,e4m3:rtn,"
-                                          "int8:weyl,int8:sr,int8:rtn,int4:weyl,int4:sr,int4:rtn",
+    ap.add_argument("--variants", default="bf16:weyl,bf16:sr,bf16:rtn,bf16:philox,"
+                                          "e4m3:weyl,e4m3:sr,e4m3:rtn,e4m3:philox,"
+                                          "int8:weyl,int8:sr,int8:rtn,int8:philox,"
+                                          "int4:weyl,int4:sr,int4:rtn",
                     help="comma-separated format:rule list; the first is the headline")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -409,7 +411,7 @@ def load_traffic(workload: str):
 
 # rocprofv3 names the update kernels k_update_slab<F, R, NT, CPT> with these codes
 _FMT_CODE = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3, "int8": 4, "int4": 5}
-_RULE_CODE = {"rtn": 0, "sr": 1, "weyl": 2}
+_RULE_CODE = {"rtn": 0, "sr": 1, "weyl": 2, "philox": 3}
 
 
 def _csv_rows(d: str, suffix: str):

@@ -45,7 +45,11 @@ typedef enum {
 typedef enum {
     SSMQ_RTN = 0,  /* round to nearest, ties to even (the native cast)                  */
     SSMQ_SR = 1,   /* stochastic: u from a counter-based hash of (seed, layer, entry, t) */
-    SSMQ_WEYL = 2  /* Weyl dither: u = top 24 bits of A(r+1)+B(c+1)+L l+S sigma+t Phi    */
+    SSMQ_WEYL = 2, /* Weyl dither: u = top 24 bits of A(r+1)+B(c+1)+L l+S sigma+t Phi    */
+    SSMQ_SR_PHILOX = 3 /* stochastic with Philox4x32-10 (the generator behind the paper's SR,
+                          Appendix B "Dithers"; Salmon et al., SC 2011): entry i at step t
+                          takes word i mod 4 of Philox(counter (i/4 mod 2^32, i/4 >> 32,
+                          t, 0), key (seed, layer)), top 24 bits                         */
 } ssmq_rule;
 
 /* Storage formats (Section 2 "Low-precision storage"; Appendix B "Formats"). */
@@ -163,6 +167,8 @@ ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t he
  *   SSMQ_SR:   top 24 bits of fmix32(i * 0x9E3779B1 + K) with the per-step key
  *              K = fmix32(fmix32(fmix32(seed) ^ layer * 0xC2B2AE3D) ^ t * 0x85EBCA77)
  *              (Appendix B "Decode regime", hash SR; fmix32 = MurmurHash3 finalizer).
+ *   SSMQ_SR_PHILOX: top 24 bits of word i mod 4 of Philox4x32-10 with counter
+ *              (floor(i/4) mod 2^32, floor(i/4) >> 32, t, 0) and key (seed, layer).
  *   SSMQ_RTN:  2^23 (u = 1/2) everywhere; nearest rounding breaks exact ties to even.
  * Arguments: n >= 0; dither_block a power of two; U24 [n] uint32 output [4 B];
  * any entry_base.

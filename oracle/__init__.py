@@ -8,7 +8,7 @@ floating-point order) and shares no code with it.
 Formats: "fp16", "bf16", "e4m3" (OCP E4M3FN with an fp32 group scale), "fp32"
 (unrounded), "int8" and "int4" (symmetric integers with an fp32 block scale; INT4
 packs two entries per byte, the even entry in the low nibble). Rules: "rtn",
-"sr", "weyl".
+"sr" (hash), "weyl", "philox" (SR from Philox4x32-10).
 
 Parity status: every function here is pinned by tests under ``tests/`` that use
 what the paper and the mathematics fix (worked values, closed forms, exact
@@ -25,7 +25,7 @@ import numpy as np
 from . import build_oracle
 
 FORMATS = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3, "int8": 4, "int4": 5}
-RULES = {"rtn": 0, "sr": 1, "weyl": 2}
+RULES = {"rtn": 0, "sr": 1, "weyl": 2, "philox": 3}
 CODE_DTYPE = {"fp16": np.uint16, "bf16": np.uint16, "e4m3": np.uint8, "fp32": np.uint32,
               "int8": np.uint8, "int4": np.uint8}
 SCALED = ("e4m3", "int8", "int4")
@@ -70,6 +70,8 @@ def lib() -> ctypes.CDLL:
     L.orc_weyl_constants.restype = None
     L.orc_fmix32.argtypes = [_u32]
     L.orc_fmix32.restype = _u32
+    L.orc_philox4x32_10.argtypes = [_vp, _vp, _vp]
+    L.orc_philox4x32_10.restype = None
     L.orc_grid.argtypes = [_int, _vp, _vp, _int]
     L.orc_grid.restype = _int
     L.orc_decode.argtypes = [_int, _u32]
@@ -112,6 +114,15 @@ def weyl_constants() -> dict:
 
 def fmix32(h: int) -> int:
     return int(lib().orc_fmix32(h & 0xFFFFFFFF))
+
+
+def philox4x32_10(ctr, key):
+    """One block of Philox4x32-10: four 32-bit words for a counter and a key."""
+    c = np.array(ctr, np.uint32)
+    k = np.array(key, np.uint32)
+    out = np.zeros(4, np.uint32)
+    lib().orc_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return [int(v) for v in out]
 
 
 def grid(fmt: str):

@@ -14,7 +14,8 @@
  *   - rounding is a neighbour search in that set followed by the threshold test
  *     of eq. (dither), carried out with exact double-precision comparisons;
  *   - thresholds are the 32-bit Weyl accumulator of Appendix B ("Dithers",
- *     hardware form) and a keyed integer hash for stochastic rounding.
+ *     hardware form), a keyed integer hash for stochastic rounding, and the
+ *     Philox4x32-10 counter-based generator for stochastic rounding.
  *
  * Floating-point order of the fused step (fp32, no contraction; this file must
  * be compiled with -ffp-contract=off):
@@ -47,7 +48,7 @@ enum { ORC_FP16 = 0, ORC_BF16 = 1, ORC_E4M3 = 2, ORC_FP32 = 3, ORC_INT8 = 4, ORC
 static int is_int(int f) { return f == ORC_INT8 || f == ORC_INT4; }
 static int int_qmax(int f) { return f == ORC_INT8 ? 127 : 7; }
 static int is_scaled(int f) { return f == ORC_E4M3 || is_int(f); }
-enum { ORC_RTN = 0, ORC_SR = 1, ORC_WEYL = 2 };
+enum { ORC_RTN = 0, ORC_SR = 1, ORC_WEYL = 2, ORC_PHILOX = 3 };
 
 /* ------------------------------------------------------------------------- */
 /* Storage formats as value sets (Section 2 "Low-precision storage";          */
@@ -312,10 +313,49 @@ static uint32_t sr_key(uint32_t seed, uint32_t layer, uint32_t t) {
     return k;
 }
 
+/*
+ * Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
+ * easy as 1, 2, 3", SC 2011), the counter-based generator behind the paper's SR
+ * (Appendix B "Dithers": torch.rand and tl.rand). Ten rounds on a counter of
+ * four 32-bit words under a two-word key; each round multiplies words 0 and 2
+ * by the round constants, mixes the high halves with the other words and the
+ * key, and the key is advanced by the Weyl increments between rounds.
+ */
+static void philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Philox SR threshold (this library's mapping): entry i at step t takes word
+ * i mod 4 of Philox4x32-10(counter = (floor(i/4) mod 2^32, floor(i/4) >> 32, t, 0),
+ * key = (seed, layer)), top 24 bits. */
+static uint32_t philox_threshold24(uint32_t seed, uint32_t layer, uint32_t t, uint64_t i) {
+    const uint64_t q = i >> 2;
+    const uint32_t ctr[4] = {(uint32_t)q, (uint32_t)(q >> 32), t, 0u};
+    const uint32_t key[2] = {seed, layer};
+    uint32_t out[4];
+    philox4x32_10(ctr, key, out);
+    return out[i & 3u] >> 8;
+}
+
 static uint32_t threshold24(int rule, uint32_t seed, uint32_t layer, uint32_t t, uint64_t i,
                             uint64_t block) {
     if (rule == ORC_WEYL) return weyl_acc(i, block, layer, seed, t) >> 8;
     if (rule == ORC_SR) return fmix32((uint32_t)i * 0x9E3779B1u + sr_key(seed, layer, t)) >> 8;
+    if (rule == ORC_PHILOX) return philox_threshold24(seed, layer, t, i);
     return 1u << 23; /* RTN: nominal u = 1/2 (rounding itself is nearest-even) */
 }
 
@@ -333,6 +373,10 @@ void orc_weyl_constants(uint32_t out[5]) {
 }
 
 uint32_t orc_fmix32(uint32_t h) { return fmix32(h); }
+
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+    philox4x32_10(ctr, key, out);
+}
 
 int orc_grid(int f, double *val, uint32_t *code, int cap) {
     ensure_init();

@@ -13,7 +13,7 @@ import torch  # imported first so the HIP runtime is the one torch already loade
 
 LIBRARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libssmq.so")
 
-RULES = {"rtn": 0, "sr": 1, "weyl": 2}
+RULES = {"rtn": 0, "sr": 1, "weyl": 2, "philox": 3}
 FORMATS = {"fp16": 0, "bf16": 1, "e4m3": 2, "fp32": 3, "int8": 4, "int4": 5}
 CODE_BYTES = {"fp16": 2, "bf16": 2, "e4m3": 1, "fp32": 4, "int8": 1, "int4": 1}
 # entries per element of the code tensor (INT4: two per byte, even entry in the low nibble)

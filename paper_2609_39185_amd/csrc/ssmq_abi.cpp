@@ -55,6 +55,9 @@ ssmq::Thr make_thr(int rule, uint32_t seed, uint32_t layer, uint32_t step, int32
                    uint32_t toff[16]) {
   ssmq::Thr th{};
   th.lb = static_cast<uint32_t>(log2i(block));
+  th.seed = seed;
+  th.layer = layer;
+  th.step = step;
   const uint32_t mask = static_cast<uint32_t>(block) - 1u;
   for (uint32_t k = 0; k < 16; ++k) {
     if (rule == SSMQ_WEYL) toff[k] = ssmq::kWeylA * (k >> th.lb) + ssmq::kWeylB * (k & mask);
@@ -75,7 +78,8 @@ ssmq::Thr make_thr(int rule, uint32_t seed, uint32_t layer, uint32_t step, int32
 
 ssmq_status check_qparams(const ssmq_qparams* q) {
   if (!q) return fail(SSMQ_EINVAL, "qparams is NULL");
-  if (q->rule < SSMQ_RTN || q->rule > SSMQ_WEYL) return fail(SSMQ_EINVAL, "unknown rule %d", q->rule);
+  if (q->rule < SSMQ_RTN || q->rule > SSMQ_SR_PHILOX)
+    return fail(SSMQ_EINVAL, "unknown rule %d", q->rule);
   if (q->format < SSMQ_FP16 || q->format > SSMQ_INT4)
     return fail(SSMQ_EINVAL, "unknown format %d", q->format);
   if (q->reserved != 0) return fail(SSMQ_EINVAL, "qparams.reserved must be 0");
@@ -260,7 +264,7 @@ ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t he
 ssmq_status ssmq_dither_fill(int32_t rule, uint32_t seed, uint32_t layer, uint32_t step,
                              uint64_t entry_base, int64_t n, int32_t dither_block,
                              uint32_t* U24, void* stream) {
-  if (rule < SSMQ_RTN || rule > SSMQ_WEYL) return fail(SSMQ_EINVAL, "unknown rule %d", rule);
+  if (rule < SSMQ_RTN || rule > SSMQ_SR_PHILOX) return fail(SSMQ_EINVAL, "unknown rule %d", rule);
   if (n < 0) return fail(SSMQ_EINVAL, "n < 0");
   if (!is_pow2(dither_block) || dither_block > (1 << 30))
     return fail(SSMQ_EINVAL, "dither_block %d is not a power of two in [1, 2^30]", dither_block);

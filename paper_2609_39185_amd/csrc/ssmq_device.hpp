@@ -45,7 +45,7 @@
 namespace ssmq {
 
 enum Fmt : int { kFP16 = 0, kBF16 = 1, kE4M3 = 2, kFP32 = 3, kINT8 = 4, kINT4 = 5 };
-enum Rule : int { kRTN = 0, kSR = 1, kWEYL = 2 };
+enum Rule : int { kRTN = 0, kSR = 1, kWEYL = 2, kPHILOX = 3 };
 
 // Weyl accumulator (Appendix B "Dithers", hardware form): 2^32 times
 // 0.7548776662, 0.5698402910, 0.1234567, 0.3141592, rounded to nearest, and the
@@ -130,6 +130,80 @@ __device__ inline uint32_t thr_word(uint32_t base, uint32_t off) {
   if constexpr (R == kWEYL) return base + off;
   else if constexpr (R == kSR) return fmix32(base + off);
   else return 0x80000000u;
+}
+
+// Philox4x32-10 (Salmon et al., SC 2011): ten rounds of two 32x32->64-bit
+// products on a four-word counter, key advanced by the Weyl increments.
+__device__ inline void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                     uint32_t k0, uint32_t k1, uint32_t (&out)[4]) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = static_cast<uint64_t>(0xD2511F53u) * c0;
+    const uint64_t p1 = static_cast<uint64_t>(0xCD9E8D57u) * c2;
+    const uint32_t n0 = static_cast<uint32_t>(p1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = static_cast<uint32_t>(p0 >> 32) ^ c3 ^ k1;
+    c1 = static_cast<uint32_t>(p1);
+    c3 = static_cast<uint32_t>(p0);
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+// Thresholds of one chunk of N entries whose first flat index is e0: tg(k) is
+// the 32-bit word of entry k (U = word >> 8). Weyl and hash SR derive it from
+// a per-chunk base and the per-position offsets; Philox SR draws word
+// (e0 + k) mod 4 of the block with counter ((e0 + k) / 4, step, 0) and key
+// (seed, layer).
+template <int R, int N>
+struct ChunkThr {
+  uint32_t base;
+  const uint32_t* off;
+  __device__ uint32_t operator()(int k) const { return thr_word<R>(base, off[k]); }
+};
+template <int N>
+struct ChunkThr<kPHILOX, N> {
+  uint32_t w[N];
+  __device__ uint32_t operator()(int k) const { return w[k]; }
+};
+
+// The 32-bit threshold word of one entry with global flat index i.
+template <int R>
+__device__ inline uint32_t entry_thr(uint64_t i, const Thr& th) {
+  if constexpr (R == kPHILOX) {
+    const uint64_t q = i >> 2;
+    uint32_t o[4];
+    philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), th.step, 0u, th.seed,
+                  th.layer, o);
+    const uint32_t j = static_cast<uint32_t>(i) & 3u;
+    return j == 0 ? o[0] : (j == 1 ? o[1] : (j == 2 ? o[2] : o[3]));
+  } else {
+    return thr_word<R>(thr_base<R>(i, th), 0u);
+  }
+}
+
+template <int R, int N>
+__device__ inline ChunkThr<R, N> chunk_thr(uint64_t e0, const Thr& th, uint32_t base,
+                                           const uint32_t* off) {
+  if constexpr (R == kPHILOX) {
+    static_assert(N % 4 == 0, "Philox blocks cover four entries");
+    ChunkThr<R, N> t;
+    const uint64_t q0 = e0 >> 2;
+#pragma unroll
+    for (int g = 0; g < N / 4; ++g) {
+      const uint64_t q = q0 + static_cast<uint64_t>(g);
+      uint32_t o[4];
+      philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), th.step, 0u,
+                    th.seed, th.layer, o);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) t.w[4 * g + i] = o[i];
+    }
+    return t;
+  } else {
+    return ChunkThr<R, N>{base, off};
+  }
 }
 
 // thr ^ signmask(x) in the top 24 bits (the low byte is don't-care).
@@ -307,9 +381,9 @@ __device__ inline bool chunk_has_nan(const float (&v)[V]) {
 // rare (the scale maps the group maximum to 448, so only its rounding error can
 // push a value past it) and take the exact path, which saturates; the
 // conversion instructions themselves do not.
-template <int F, int R>
-__device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t base,
-                                       const uint32_t* off, bool maybe_nan, bool may_saturate) {
+template <int F, int R, typename TG>
+__device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG& tg,
+                                       bool maybe_nan, bool may_saturate) {
   constexpr int V = Traits<F>::V;
   uint32_t w[4];
   if constexpr (F == kFP32) {
@@ -326,10 +400,10 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
       } else {
         // Both halves are written, so the destination's previous contents are
         // don't-care: it starts as the first threshold, which dies here.
-        const uint32_t t0 = signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]);
+        const uint32_t t0 = signed_thr(tg(2 * i), v[2 * i]);
         p = __builtin_amdgcn_cvt_sr_bf16_f32(__builtin_bit_cast(v2bf, t0), v[2 * i], t0, false);
         p = __builtin_amdgcn_cvt_sr_bf16_f32(
-            p, v[2 * i + 1], signed_thr(thr_word<R>(base, off[2 * i + 1]), v[2 * i + 1]), true);
+            p, v[2 * i + 1], signed_thr(tg(2 * i + 1), v[2 * i + 1]), true);
       }
       w[i] = __builtin_bit_cast(uint32_t, p);
     }
@@ -340,10 +414,10 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
       if constexpr (R == kRTN) {
         p = (v2h){static_cast<_Float16>(v[2 * i]), static_cast<_Float16>(v[2 * i + 1])};
       } else {
-        const uint32_t t0 = signed_thr(thr_word<R>(base, off[2 * i]), v[2 * i]);
+        const uint32_t t0 = signed_thr(tg(2 * i), v[2 * i]);
         p = __builtin_amdgcn_cvt_sr_f16_f32(__builtin_bit_cast(v2h, t0), v[2 * i], t0, false);
         p = __builtin_amdgcn_cvt_sr_f16_f32(
-            p, v[2 * i + 1], signed_thr(thr_word<R>(base, off[2 * i + 1]), v[2 * i + 1]), true);
+            p, v[2 * i + 1], signed_thr(tg(2 * i + 1), v[2 * i + 1]), true);
       }
       w[i] = __builtin_bit_cast(uint32_t, p);
     }
@@ -357,11 +431,11 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
         d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k], q[k + 1], static_cast<int>(__float_as_uint(q[k])), false);
         d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k + 2], q[k + 3], d, true);
       } else {
-        const uint32_t t0 = signed_thr(thr_word<R>(base, off[k]), q[k]);  // dies here
+        const uint32_t t0 = signed_thr(tg(k), q[k]);  // dies here
         d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k], t0, static_cast<int>(t0), 0);
-        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 1], signed_thr(thr_word<R>(base, off[k + 1]), q[k + 1]), d, 1);
-        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 2], signed_thr(thr_word<R>(base, off[k + 2]), q[k + 2]), d, 2);
-        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 3], signed_thr(thr_word<R>(base, off[k + 3]), q[k + 3]), d, 3);
+        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 1], signed_thr(tg(k + 1), q[k + 1]), d, 1);
+        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 2], signed_thr(tg(k + 2), q[k + 2]), d, 2);
+        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 3], signed_thr(tg(k + 3), q[k + 3]), d, 3);
       }
       w[i] = static_cast<uint32_t>(d);
     }
@@ -369,7 +443,7 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], uint32_t 
   if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, V>(v, maybe_nan, may_saturate)) != 0) {
 #pragma unroll
     for (int k = 0; k < V; ++k) {
-      if (needs_exact_path<F, R>(v[k])) patch_code<F>(w, k, round_code<F, R>(v[k], thr_word<R>(base, off[k])));
+      if (needs_exact_path<F, R>(v[k])) patch_code<F>(w, k, round_code<F, R>(v[k], tg(k)));
     }
   }
   return make_uint4(w[0], w[1], w[2], w[3]);
@@ -388,10 +462,9 @@ __device__ inline uint32_t pack_bytes(uint32_t w0, uint32_t w1, uint32_t w2, uin
 // r24 = 2^24 r of their group (r24 is infinite when 2^24 r overflows).
 // may_saturate: fl32(max|h| r24) > qmax 2^24 (RTN: fl32(max|h| r) > qmax)
 // somewhere in the chunk; maybe_nan: a NaN may be among h.
-template <int F, int R>
+template <int F, int R, typename TG>
 __device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, float r24,
-                                               uint32_t base, const uint32_t* off,
-                                               bool maybe_nan, bool may_saturate) {
+                                               const TG& tg, bool maybe_nan, bool may_saturate) {
   constexpr float qmax = Traits<F>::qmax;
   uint32_t S[16];
   bool rare = maybe_nan || may_saturate;
@@ -405,7 +478,7 @@ __device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, f
       const float q24 = h[k] * r24;
       mn = fminf(mn, __builtin_fabsf(q24));
       S[k] = static_cast<uint32_t>(static_cast<int>(__builtin_floorf(q24))) +
-             (thr_word<R>(base, off[k]) >> 8);
+             (tg(k) >> 8);
     }
     rare = rare || !(mn >= 0x1p-102f);
   }
@@ -435,7 +508,7 @@ __device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, f
         const float a24 = __builtin_fabsf(h[k] * r24);
         exact = !(a24 >= 0x1p-102f && a24 <= qmax * 0x1p24f);
       }
-      if (exact) patch_code<F>(w, k, round_code<F, R>(h[k] * r, thr_word<R>(base, off[k])));
+      if (exact) patch_code<F>(w, k, round_code<F, R>(h[k] * r, tg(k)));
     }
   }
   if constexpr (F == kINT8) return make_uint4(w[0], w[1], w[2], w[3]);
@@ -454,18 +527,18 @@ __device__ inline bool saturates(float m, float r) {
 
 // One chunk of fp32 values h -> codes, for every format: r = 1 / s of the
 // chunk's group (ignored by unscaled formats).
-template <int F, int R>
-__device__ inline chunk_t<F> quantize_any(const float (&h)[Traits<F>::V], float r, uint32_t base,
-                                         const uint32_t* off, bool maybe_nan, bool sat) {
+template <int F, int R, typename TG>
+__device__ inline chunk_t<F> quantize_any(const float (&h)[Traits<F>::V], float r, const TG& tg,
+                                         bool maybe_nan, bool sat) {
   if constexpr (is_int_fmt<F>) {
-    return quantize_int_chunk<F, R>(h, r, r * 0x1p24f, base, off, maybe_nan, sat);
+    return quantize_int_chunk<F, R>(h, r, r * 0x1p24f, tg, maybe_nan, sat);
   } else if constexpr (F == kE4M3) {
     float v[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k) v[k] = h[k] * r;
-    return quantize_chunk<F, R>(v, base, off, maybe_nan, sat);
+    return quantize_chunk<F, R>(v, tg, maybe_nan, sat);
   } else {
-    return quantize_chunk<F, R>(h, base, off, maybe_nan, sat);
+    return quantize_chunk<F, R>(h, tg, maybe_nan, sat);
   }
 }
 

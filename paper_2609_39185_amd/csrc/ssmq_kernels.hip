@@ -183,7 +183,9 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
     const uint32_t base = (j == 0) ? base0
                           : (a.pass_thr_ok ? base0 + static_cast<uint32_t>(j) * a.pass_thr_inc
                                            : thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr));
-    const chunk_t<F> out = quantize_any<F, R>(h[j], r[j], base, a.toff, bad[j], sat[j]);
+    const chunk_t<F> out = quantize_any<F, R>(
+        h[j], r[j], chunk_thr<R, V>(a.entry_base + static_cast<uint64_t>(e), a.thr, base, a.toff),
+        bad[j], sat[j]);
     store_stream(hstate + chunk_bytes_at<F>(l0 + j * pass), out);
   }
 }
@@ -253,7 +255,9 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
     if (live && (t & (a.lanes_per_group - 1)) == 0) a.scale[e >> a.group_shift] = s;
     sat = saturates<F, R>(m, rs);
   }
-  const chunk_t<F> out = quantize_any<F, R>(h, rs, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr), a.toff, bad, sat);
+  const uint64_t ge = a.entry_base + static_cast<uint64_t>(e);
+  const chunk_t<F> out =
+      quantize_any<F, R>(h, rs, chunk_thr<R, V>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff), bad, sat);
   if (live) store_stream(state + chunk_bytes_at<F>(e), out);
 }
 
@@ -279,12 +283,13 @@ __global__ __launch_bounds__(256) void k_requant(RequantArgs a) {
   if (e + V <= a.n) {
     float h[V];
     load_floats<V>(a.h + e, h);
-    const uint4 out = quantize_chunk<F, R>(h, thr_base<R>(ge, a.thr), a.toff, chunk_has_nan<V>(h), false);
+    const uint4 out = quantize_chunk<F, R>(h, chunk_thr<R, V>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff),
+                                           chunk_has_nan<V>(h), false);
     *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + chunk_bytes_at<F>(e)) = out;
   } else {
     for (int64_t k = e; k < a.n; ++k) {
       const uint64_t gk = a.entry_base + static_cast<uint64_t>(k);
-      store_code<F>(a.codes, k, round_code<F, R>(a.h[k], thr_word<R>(thr_base<R>(gk, a.thr), 0u)));
+      store_code<F>(a.codes, k, round_code<F, R>(a.h[k], entry_thr<R>(gk, a.thr)));
     }
   }
 }
@@ -331,8 +336,9 @@ __global__ __launch_bounds__(256) void k_requant_scaled(RequantArgs a) {
       float mc = 0.0f;
 #pragma unroll
       for (int k = 0; k < 16; ++k) mc = fmaxf(mc, __builtin_fabsf(h[k]));
-      const chunk_t<F> out = quantize_any<F, R>(h, rs, thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr),
-                                                a.toff, chunk_has_nan<16>(h), saturates<F, R>(mc, rs));
+      const uint64_t ge = a.entry_base + static_cast<uint64_t>(e);
+      const chunk_t<F> out = quantize_any<F, R>(h, rs, chunk_thr<R, 16>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff),
+                                                chunk_has_nan<16>(h), saturates<F, R>(mc, rs));
       if (ok) *reinterpret_cast<chunk_t<F>*>(static_cast<uint8_t*>(a.codes) + chunk_bytes_at<F>(e)) = out;
     }
   }
@@ -346,7 +352,7 @@ __global__ __launch_bounds__(256) void k_dither_fill(DitherArgs a) {
   const int64_t lim = (a.n - e < 4) ? (a.n - e) : 4;
   for (int64_t k = 0; k < lim; ++k) {
     const uint64_t ge = a.entry_base + static_cast<uint64_t>(e + k);
-    a.out[e + k] = (R == kRTN) ? (1u << 23) : (thr_word<R>(thr_base<R>(ge, a.thr), 0u) >> 8);
+    a.out[e + k] = (R == kRTN) ? (1u << 23) : (entry_thr<R>(ge, a.thr) >> 8);
   }
 }
 
@@ -397,6 +403,7 @@ static hipError_t launch_update_f(const UpdateArgs& a, int rule, int cfg, bool a
   switch (rule) {
     case kRTN: return launch_update_fr<F, kRTN>(a, cfg, aps, s);
     case kSR: return launch_update_fr<F, kSR>(a, cfg, aps, s);
+    case kPHILOX: return launch_update_fr<F, kPHILOX>(a, cfg, aps, s);
     default: return launch_update_fr<F, kWEYL>(a, cfg, aps, s);
   }
 }
@@ -421,6 +428,7 @@ static hipError_t launch_requant_f(const RequantArgs& a, int rule, hipStream_t s
   switch (rule) {
     case kRTN: hipLaunchKernelGGL((k_requant<F, kRTN>), dim3(grid), dim3(256), 0, s, a); break;
     case kSR: hipLaunchKernelGGL((k_requant<F, kSR>), dim3(grid), dim3(256), 0, s, a); break;
+    case kPHILOX: hipLaunchKernelGGL((k_requant<F, kPHILOX>), dim3(grid), dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((k_requant<F, kWEYL>), dim3(grid), dim3(256), 0, s, a); break;
   }
   return hipGetLastError();
@@ -436,6 +444,7 @@ static hipError_t launch_requant_scaled(const RequantArgs& a, int rule, hipStrea
   switch (rule) {
     case kRTN: hipLaunchKernelGGL((k_requant_scaled<F, kRTN>), dim3(grid), dim3(256), 0, s, a); break;
     case kSR: hipLaunchKernelGGL((k_requant_scaled<F, kSR>), dim3(grid), dim3(256), 0, s, a); break;
+    case kPHILOX: hipLaunchKernelGGL((k_requant_scaled<F, kPHILOX>), dim3(grid), dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((k_requant_scaled<F, kWEYL>), dim3(grid), dim3(256), 0, s, a); break;
   }
   return hipGetLastError();
@@ -458,6 +467,7 @@ hipError_t launch_dither(const DitherArgs& a, int rule, hipStream_t s) {
   switch (rule) {
     case kRTN: hipLaunchKernelGGL((k_dither_fill<kRTN>), dim3(grid), dim3(256), 0, s, a); break;
     case kSR: hipLaunchKernelGGL((k_dither_fill<kSR>), dim3(grid), dim3(256), 0, s, a); break;
+    case kPHILOX: hipLaunchKernelGGL((k_dither_fill<kPHILOX>), dim3(grid), dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((k_dither_fill<kWEYL>), dim3(grid), dim3(256), 0, s, a); break;
   }
   return hipGetLastError();

@@ -11,6 +11,7 @@ namespace ssmq {
 struct Thr {
   uint32_t key;  // Weyl: A + B + L*layer + S*seed + Phi*t; SR: per-step key
   uint32_t lb;   // log2(dither_block)
+  uint32_t seed, layer, step;  // Philox SR: key (seed, layer), counter word 2 = step
 };
 
 // Division of 32-bit unsigned integers by an invariant d >= 1 with one high

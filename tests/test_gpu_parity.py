@@ -29,7 +29,7 @@ def ssmq():
 # --------------------------------------------------------------------------
 # thresholds
 # --------------------------------------------------------------------------
-@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl", "philox"])
 @pytest.mark.parametrize("block", [1, 16, 128, 1 << 20])
 @pytest.mark.parametrize("entry_base,n", [(0, 0), (0, 1), (3, 1000), (2 ** 33 + 7, 4099),
                                           (1 << 20, 65536)])
@@ -79,7 +79,7 @@ def _edge_values(fmt, rng, n_random, entry_base, rule, block, seed, layer, step)
 
 
 @pytest.mark.parametrize("fmt", ["fp16", "bf16", "fp32"])
-@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl", "philox"])
 @pytest.mark.parametrize("n,entry_base,block", [(16 * 4096, 0, 16), (100_003, 48, 128),
                                                 (15, 16, 1), (0, 0, 16)])
 def test_requantize_bit_exact(ssmq, fmt, rule, n, entry_base, block):
@@ -101,7 +101,7 @@ def test_requantize_bit_exact(ssmq, fmt, rule, n, entry_base, block):
         assert np.array_equal(got, want), np.nonzero(got != want)[0][:10]
 
 
-@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl", "philox"])
 @pytest.mark.parametrize("group,n_groups", [(16, 700), (128, 300), (8192, 9), (48, 33),
                                             (2048, 5)])
 def test_requantize_e4m3_bit_exact(ssmq, rule, group, n_groups):
@@ -142,6 +142,19 @@ M2_SMALL = ("mamba2", 2, 4, 64, 128, 2)
                                    ("e4m3", {"scale_group": 1024, "dither_block": 1})])
 def test_step_head_tile(ssmq, rule, fmt, q):
     check_step(fmt, rule, *M2_SMALL, seed=10, what="head tile", step=5, layer=2, **q)
+
+
+@pytest.mark.parametrize("fmt,q", [("bf16", {"dither_block": 128}), ("fp16", {"dither_block": 16}),
+                                   ("e4m3", {"dither_block": 128}), ("e4m3", {"scale_group": 128}),
+                                   ("int8", {"scale_group": 128}), ("int4", {"scale_group": 16})])
+def test_step_head_tile_philox(ssmq, fmt, q):
+    """SR driven by Philox4x32-10 (the generator behind the paper's SR)."""
+    check_step(fmt, "philox", *M2_SMALL, seed=12, what="philox head tile", step=7, layer=3, **q)
+
+
+def test_step_philox_mamba1_rows(ssmq):
+    check_step("fp16", "philox", "mamba1", 3, 200, 1, 16, 1, seed=13, what="philox rows",
+               step=11, layer=2)
 
 
 SHAPES = [

@@ -224,7 +224,7 @@ def test_decay_bound(orc):
             assert abs(e_T) <= max(abs(r) for r in tails)
 
 
-@pytest.mark.parametrize("rule", ["sr", "weyl"])
+@pytest.mark.parametrize("rule", ["sr", "weyl", "philox"])
 def test_dithers_are_unbiased(orc, rule):
     """E[Q(x)] = x: averaged over steps, the stored value of a fixed x converges to x."""
     rng = np.random.default_rng(17)
@@ -235,7 +235,7 @@ def test_dithers_are_unbiased(orc, rule):
         U = orc.thresholds(rule, 0, 0, t, 0, 64, 16)
         acc += orc.decode("fp16", orc.round_values("fp16", rule, x, U))
     bias = (acc / T - x.astype(np.float64)) / 2.0 ** -10
-    tol = 4 * 0.5 / np.sqrt(T) if rule == "sr" else 0.01
+    tol = 4 * 0.5 / np.sqrt(T) if rule in ("sr", "philox") else 0.01
     assert np.all(np.abs(bias) < tol)
 
 

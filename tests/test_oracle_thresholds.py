@@ -167,3 +167,47 @@ def test_sr_keys_differ_by_seed_layer_step(orc):
 
 def test_rtn_nominal_threshold(orc):
     assert np.all(orc.thresholds("rtn", 5, 5, 5, 0, 64, 16) == 1 << 23)
+
+
+# --------------------------------------------------------------------------
+# Philox4x32-10 SR (the generator behind the paper's SR, Appendix B "Dithers")
+# --------------------------------------------------------------------------
+# Known-answer vectors of Philox4x32-10 published with the Random123 library
+# (Salmon et al., SC 2011): (counter, key) -> output.
+PHILOX_KAT = [
+    ((0, 0, 0, 0), (0, 0), (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+    ((0xFFFFFFFF,) * 4, (0xFFFFFFFF,) * 2, (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+    ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+     (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+]
+
+
+@pytest.mark.parametrize("ctr,key,want", PHILOX_KAT)
+def test_philox_known_answers(orc, ctr, key, want):
+    assert tuple(orc.philox4x32_10(ctr, key)) == want
+
+
+def test_philox_threshold_mapping(orc):
+    """Entry i, step t: word i mod 4 of Philox(counter (i/4 lo, i/4 hi, t, 0), key (seed, layer))."""
+    seed, layer, t = 7, 3, 41
+    base = 2 ** 34 + 8
+    got = orc.thresholds("philox", seed, layer, t, base, 12, 16)
+    for k in range(12):
+        i = base + k
+        q = i >> 2
+        words = orc.philox4x32_10((q & 0xFFFFFFFF, q >> 32, t, 0), (seed, layer))
+        assert got[k] == words[i & 3] >> 8
+
+
+def test_philox_moments_and_keys(orc):
+    n = 1 << 18
+    u = orc.thresholds("philox", 0, 0, 5, 0, n, 16) / TWO24
+    m, v, r = _moments(u)
+    assert abs(m - 0.5) < 5 / np.sqrt(12 * n) and abs(v - 1 / 12) < 1e-3 and abs(r) < 5 / np.sqrt(n)
+    T = 1 << 13
+    over_time = np.array([orc.thresholds("philox", 1, 3, t, 777, 1, 16)[0] for t in range(T)]) / TWO24
+    m, v, r = _moments(over_time)
+    assert abs(m - 0.5) < 5 / np.sqrt(12 * T) and abs(v - 1 / 12) < 4e-3 and abs(r) < 5 / np.sqrt(T)
+    base = orc.thresholds("philox", 0, 0, 0, 0, 4096, 16)
+    for args in ((1, 0, 0), (0, 1, 0), (0, 0, 1)):
+        assert np.mean(base == orc.thresholds("philox", *args, 0, 4096, 16)) < 0.01
