@@ -20,16 +20,17 @@
 //   bf16  nothing (k = 16 everywhere; NaN and Inf come out canonical);
 //   fp16  the subnormal range |x| < 2^-14 (the conversion is not exact there);
 //   E4M3  NaN (the conversion loses its sign) and |q| < 2^-10, where k > 24.
-// E4M3 values above 448 (saturation) also take the exact path; the conversions
-// do not saturate above 464.
+// E4M3 values are clamped to +-448 (saturation) before the stochastic
+// conversions, which do not saturate.
 //
 // INT8 / INT4 (symmetric, block scale, Appendix B "Formats") round q = h / s
 // on the integer lattice. With q24 = h * (2^24 / s) (exactly q * 2^24 whenever
 // q is a normal float), X = floor(q24) and U the 24-bit threshold,
 // floor(q + U / 2^24) = (X + U) >> 24 exactly: only the top 24 fraction bits of
 // q can decide the comparison with a multiple of 2^-24. The low byte (nibble)
-// of X + U shifted right by 24 is the stored code. Values beyond +-qmax, NaN
-// and |q| < 2^-126 (q24 then differs from q * 2^24) take the exact path.
+// of X + U shifted right by 24 is the stored code. Values are clamped to
+// +-qmax first (the bounds are lattice points, so this is the saturation);
+// NaN and |q| < 2^-126 (q24 then differs from q * 2^24) take the exact path.
 //
 // Exact software path. Normal ranges use the carry rule on the magnitude bits.
 // Below the smallest normal of fp16 and E4M3 the grid step is fixed, |x| / step
@@ -77,17 +78,18 @@ template <int F> struct Traits;
 template <> struct Traits<kFP16> { static constexpr int V = 8, CB = 16; static constexpr bool scaled = false; };
 template <> struct Traits<kBF16> { static constexpr int V = 8, CB = 16; static constexpr bool scaled = false; };
 template <> struct Traits<kFP32> { static constexpr int V = 4, CB = 16; static constexpr bool scaled = false; };
+// zh = fl32(1 / qmax) and zl = fl32(1 / qmax - zh) serve the group-scale division.
 template <> struct Traits<kE4M3> {
   static constexpr int V = 16, CB = 16; static constexpr bool scaled = true;
-  static constexpr float qmax = 448.0f;
+  static constexpr float qmax = 448.0f, zh = 0x1.24924ap-9f, zl = -0x1.b6db6ep-34f;
 };
 template <> struct Traits<kINT8> {
   static constexpr int V = 16, CB = 16; static constexpr bool scaled = true;
-  static constexpr float qmax = 127.0f;
+  static constexpr float qmax = 127.0f, zh = 0x1.020408p-7f, zl = 0x1.020408p-35f;
 };
 template <> struct Traits<kINT4> {
   static constexpr int V = 16, CB = 8; static constexpr bool scaled = true;
-  static constexpr float qmax = 7.0f;
+  static constexpr float qmax = 7.0f, zh = 0x1.24924ap-3f, zl = -0x1.b6db6ep-28f;
 };
 template <int F> constexpr bool is_int_fmt = (F == kINT8 || F == kINT4);
 
@@ -339,9 +341,8 @@ __device__ inline void patch_code(uint32_t (&w)[4], int k, uint32_t c) {
 template <int F, int R>
 __device__ inline bool needs_exact_path(float v) {
   if constexpr (F == kE4M3) {
-    const float m = __builtin_fabsf(v);
-    if constexpr (R == kRTN) return !(m <= 448.0f);                    // NaN or saturation
-    else return !(m >= 0x1p-10f && m <= 448.0f);                      // NaN, k > 24, saturation
+    if constexpr (R == kRTN) return v != v;                            // NaN
+    else return !(__builtin_fabsf(v) >= 0x1p-10f);                     // NaN or k > 24
   } else if constexpr (F == kFP16) {
     if constexpr (R == kRTN) return false;
     else return __builtin_fabsf(v) < 0x1p-14f;                         // subnormal range
@@ -350,21 +351,20 @@ __device__ inline bool needs_exact_path(float v) {
   }
 }
 
-// Does any value of the chunk need the exact path? maybe_nan and may_saturate
-// come from the caller (a NaN, or for E4M3 a magnitude above 448, anywhere in
-// the chunk; either may be a false alarm); the small-magnitude tests use the
-// chunk minimum (fminf ignores NaN).
+// Does any value of the chunk need the exact path? maybe_nan comes from the
+// caller (a NaN anywhere in the chunk, possibly a false alarm); the small-
+// magnitude tests use the chunk minimum (fminf ignores NaN).
 template <int F, int R, int V>
-__device__ inline bool chunk_is_rare(const float (&v)[V], bool maybe_nan, bool may_saturate) {
+__device__ inline bool chunk_is_rare(const float (&v)[V], bool maybe_nan) {
   if constexpr (F == kBF16 || F == kFP32) return false;
   else if constexpr (F == kFP16 && R == kRTN) return false;
-  else if constexpr (F == kE4M3 && R == kRTN) return maybe_nan || may_saturate;
+  else if constexpr (F == kE4M3 && R == kRTN) return maybe_nan;
   else {
     float mn = __builtin_fabsf(v[0]);
 #pragma unroll
     for (int k = 1; k < V; ++k) mn = fminf(mn, __builtin_fabsf(v[k]));
     if constexpr (F == kFP16) return mn < 0x1p-14f;
-    else return maybe_nan || may_saturate || !(mn >= 0x1p-10f);
+    else return maybe_nan || !(mn >= 0x1p-10f);
   }
 }
 
@@ -377,13 +377,14 @@ __device__ inline bool chunk_has_nan(const float (&v)[V]) {
   return n;
 }
 
-// may_saturate (E4M3): some |v| of the chunk may exceed 448. Such entries are
-// rare (the scale maps the group maximum to 448, so only its rounding error can
-// push a value past it) and take the exact path, which saturates; the
-// conversion instructions themselves do not.
+// E4M3 values can exceed 448 only by the scale's own rounding (the scale maps
+// the group maximum to 448): the stochastic conversions, which do not saturate,
+// get values clamped with v_med3_f32 (clamping first is eq. (dither) on the
+// saturated grid); round-to-nearest needs no clamp below 464, which a scaled
+// value never reaches.
 template <int F, int R, typename TG>
 __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG& tg,
-                                       bool maybe_nan, bool may_saturate) {
+                                       bool maybe_nan) {
   constexpr int V = Traits<F>::V;
   uint32_t w[4];
   if constexpr (F == kFP32) {
@@ -422,7 +423,10 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG&
       w[i] = __builtin_bit_cast(uint32_t, p);
     }
   } else {  // E4M3, values already scaled
-    const float (&q)[V] = v;
+    float q[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+      q[k] = (R == kRTN) ? v[k] : __builtin_amdgcn_fmed3f(v[k], -448.0f, 448.0f);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int k = 4 * i;
@@ -440,7 +444,7 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG&
       w[i] = static_cast<uint32_t>(d);
     }
   }
-  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, V>(v, maybe_nan, may_saturate)) != 0) {
+  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, V>(v, maybe_nan)) != 0) {
 #pragma unroll
     for (int k = 0; k < V; ++k) {
       if (needs_exact_path<F, R>(v[k])) patch_code<F>(w, k, round_code<F, R>(v[k], tg(k)));
@@ -459,28 +463,33 @@ __device__ inline uint32_t pack_bytes(uint32_t w0, uint32_t w1, uint32_t w2, uin
 }
 
 // INT8 / INT4 chunk of 16 entries. h: the fp32 values, r = fl32(1 / s) and
-// r24 = 2^24 r of their group (r24 is infinite when 2^24 r overflows).
-// may_saturate: fl32(max|h| r24) > qmax 2^24 (RTN: fl32(max|h| r) > qmax)
-// somewhere in the chunk; maybe_nan: a NaN may be among h.
+// r24 = 2^24 r of their group (r24 is infinite when 2^24 r overflows);
+// maybe_nan: a NaN may be among h. Values are clamped to +-qmax before the
+// floor (the bounds are lattice points, so this is the exact saturation).
 template <int F, int R, typename TG>
 __device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, float r24,
-                                               const TG& tg, bool maybe_nan, bool may_saturate) {
+                                               const TG& tg, bool maybe_nan) {
   constexpr float qmax = Traits<F>::qmax;
   uint32_t S[16];
-  bool rare = maybe_nan || may_saturate;
+  bool rare = maybe_nan;
   if constexpr (R == kRTN) {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) S[k] = static_cast<uint32_t>(static_cast<int>(__builtin_rintf(h[k] * r)));
+    for (int k = 0; k < 16; ++k)
+      S[k] = static_cast<uint32_t>(static_cast<int>(
+          __builtin_rintf(__builtin_amdgcn_fmed3f(h[k] * r, -qmax, qmax))));
   } else {
     float mn = __builtin_inff();
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       const float q24 = h[k] * r24;
       mn = fminf(mn, __builtin_fabsf(q24));
-      S[k] = static_cast<uint32_t>(static_cast<int>(__builtin_floorf(q24))) +
-             (tg(k) >> 8);
+      int X;  // floor of the clamped value
+      asm("v_cvt_flr_i32_f32 %0, %1"
+          : "=v"(X)
+          : "v"(__builtin_amdgcn_fmed3f(q24, -qmax * 0x1p24f, qmax * 0x1p24f)));
+      S[k] = static_cast<uint32_t>(X) + (tg(k) >> 8);
     }
-    rare = rare || !(mn >= 0x1p-102f);
+    rare = rare || !(mn >= 0x1p-102f) || !(r24 < __builtin_inff());
   }
   constexpr int B = (R == kRTN) ? 0 : 3;  // the byte that holds the code
   uint32_t w[4];
@@ -503,10 +512,10 @@ __device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, f
     for (int k = 0; k < 16; ++k) {
       bool exact;
       if constexpr (R == kRTN) {
-        exact = !(__builtin_fabsf(h[k] * r) <= qmax);
+        exact = h[k] != h[k];
       } else {
-        const float a24 = __builtin_fabsf(h[k] * r24);
-        exact = !(a24 >= 0x1p-102f && a24 <= qmax * 0x1p24f);
+        // NaN, q below the normal range (q24 then differs from q 2^24), or r24 overflowed
+        exact = !(__builtin_fabsf(h[k] * r24) >= 0x1p-102f) || !(r24 < __builtin_inff());
       }
       if (exact) patch_code<F>(w, k, round_code<F, R>(h[k] * r, tg(k)));
     }
@@ -515,30 +524,20 @@ __device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, f
   else return make_uint2(w[0], w[1]);
 }
 
-// Whether some value of a chunk whose largest magnitude is m can exceed qmax
-// once scaled by r (fp32 multiplication is monotone, so the maximum decides).
-// The dithered INT path scales by r24 = 2^24 r and is checked on that product,
-// which also flags an r24 that overflowed.
-template <int F, int R>
-__device__ inline bool saturates(float m, float r) {
-  if constexpr (is_int_fmt<F> && R != kRTN) return m * (r * 0x1p24f) > Traits<F>::qmax * 0x1p24f;
-  else return m * r > Traits<F>::qmax;
-}
-
 // One chunk of fp32 values h -> codes, for every format: r = 1 / s of the
 // chunk's group (ignored by unscaled formats).
 template <int F, int R, typename TG>
 __device__ inline chunk_t<F> quantize_any(const float (&h)[Traits<F>::V], float r, const TG& tg,
-                                         bool maybe_nan, bool sat) {
+                                         bool maybe_nan) {
   if constexpr (is_int_fmt<F>) {
-    return quantize_int_chunk<F, R>(h, r, r * 0x1p24f, tg, maybe_nan, sat);
+    return quantize_int_chunk<F, R>(h, r, r * 0x1p24f, tg, maybe_nan);
   } else if constexpr (F == kE4M3) {
     float v[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k) v[k] = h[k] * r;
-    return quantize_chunk<F, R>(v, tg, maybe_nan, sat);
+    return quantize_chunk<F, R>(v, tg, maybe_nan);
   } else {
-    return quantize_chunk<F, R>(h, tg, maybe_nan, sat);
+    return quantize_chunk<F, R>(h, tg, maybe_nan);
   }
 }
 
@@ -587,11 +586,29 @@ __device__ inline void decode_chunk(const uint4& raw, float (&out)[Traits<F>::V]
 }
 
 // Group scale of a scaled format: s = fl32(m / qmax), flushed to zero below
-// 2^-126.
+// 2^-126. For m in [2^-112, FLT_MAX], fma(m, zh, fl32(m zl)) is the correctly
+// rounded quotient (Brisebarre, Muller and Raina, "Accelerating correctly rounded
+// floating-point division when the divisor is known in advance", 2004; checked
+// here for every such fp32 m and qmax = 7, 127, 448); smaller or infinite m
+// divide (a wave-uniform branch, taken only by waves that hold such a group).
 template <int F>
 __device__ inline float group_scale(float m) {
-  const float s = m / Traits<F>::qmax;
+  float s = fmaf(m, Traits<F>::zh, m * Traits<F>::zl);
+  const bool slow = !(m >= 0x1p-112f && m <= 3.40282347e38f);
+  if (__builtin_amdgcn_ballot_w64(slow) != 0) {
+    if (slow) s = m / Traits<F>::qmax;
+  }
   return (s >= 1.17549435e-38f) ? s : 0.0f;
+}
+
+// r = fl32(1 / s) for a group scale s: 0 for s = 0 or s infinite; otherwise
+// s lies in [2^-126, 2^126), where one Newton step from v_rcp_f32,
+// fma(fma(-s, y0, 1), y0, y0), is the correctly rounded reciprocal (checked on
+// the device for every fp32 value in that range).
+__device__ inline float recip_scale(float s) {
+  const float y0 = __builtin_amdgcn_rcpf(s);
+  const float r = fmaf(fmaf(-s, y0, 1.0f), y0, y0);
+  return (s > 0.0f && s < __builtin_inff()) ? r : 0.0f;
 }
 
 // ---------------------------------------------------------------------------

@@ -126,10 +126,9 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
     if (cc == 0) hy[r0 + j * rows_per_pass] = ys + Dv * xv[j];
   }
 
-  float r[CPT];
-  bool sat[CPT];  // scaled formats: some |q| of the chunk may exceed qmax
+  float r[CPT];  // scaled formats: 1 / s of each chunk's group
 #pragma unroll
-  for (int j = 0; j < CPT; ++j) { r[j] = 1.0f; sat[j] = false; }
+  for (int j = 0; j < CPT; ++j) r[j] = 1.0f;
   if constexpr (Traits<F>::scaled) {
     // Lane maxima of |h| ignore NaN and are >= 0, so the cross-lane maximum can
     // compare bit patterns as unsigned integers.
@@ -156,7 +155,7 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
         const float s = group_scale<F>(__uint_as_float(w));
         if (t == 0) {
           sh[0] = s;
-          sh[1] = (s == 0.0f) ? 0.0f : 1.0f / s;
+          sh[1] = recip_scale(s);
           a.scale[tile] = s;
         }
       }
@@ -168,12 +167,10 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
 #pragma unroll
       for (int j = 0; j < CPT; ++j) {
         const float s = group_scale<F>(__uint_as_float(lane_umax(m[j], a.lanes_per_group)));
-        r[j] = (s == 0.0f) ? 0.0f : 1.0f / s;
+        r[j] = recip_scale(s);
         if ((t & (a.lanes_per_group - 1)) == 0) a.scale[(e0 + j * pass) >> a.group_shift] = s;
       }
     }
-#pragma unroll
-    for (int j = 0; j < CPT; ++j) sat[j] = saturates<F, R>(__uint_as_float(m[j]), r[j]);
   }
 
   const uint32_t base0 = thr_base<R>(a.entry_base + static_cast<uint64_t>(e0), a.thr);
@@ -185,7 +182,7 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
                                            : thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr));
     const chunk_t<F> out = quantize_any<F, R>(
         h[j], r[j], chunk_thr<R, V>(a.entry_base + static_cast<uint64_t>(e), a.thr, base, a.toff),
-        bad[j], sat[j]);
+        bad[j]);
     store_stream(hstate + chunk_bytes_at<F>(l0 + j * pass), out);
   }
 }
@@ -244,20 +241,18 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   const bool bad = !__builtin_isfinite(ys);
   ys = lane_sum(ys, a.lanes_per_row);
   if (live && cc == 0) a.y[row] = ys + Dv * xv;
-  bool sat = false;
   float rs = 1.0f;
   if constexpr (Traits<F>::scaled) {
     float m = 0.0f;
 #pragma unroll
     for (int k = 0; k < V; ++k) m = fmaxf(m, __builtin_fabsf(h[k]));
     const float s = group_scale<F>(__uint_as_float(lane_umax(__float_as_uint(m), a.lanes_per_group)));
-    rs = (s == 0.0f) ? 0.0f : 1.0f / s;
+    rs = recip_scale(s);
     if (live && (t & (a.lanes_per_group - 1)) == 0) a.scale[e >> a.group_shift] = s;
-    sat = saturates<F, R>(m, rs);
   }
   const uint64_t ge = a.entry_base + static_cast<uint64_t>(e);
   const chunk_t<F> out =
-      quantize_any<F, R>(h, rs, chunk_thr<R, V>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff), bad, sat);
+      quantize_any<F, R>(h, rs, chunk_thr<R, V>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff), bad);
   if (live) store_stream(state + chunk_bytes_at<F>(e), out);
 }
 
@@ -284,7 +279,7 @@ __global__ __launch_bounds__(256) void k_requant(RequantArgs a) {
     float h[V];
     load_floats<V>(a.h + e, h);
     const uint4 out = quantize_chunk<F, R>(h, chunk_thr<R, V>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff),
-                                           chunk_has_nan<V>(h), false);
+                                           chunk_has_nan<V>(h));
     *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.codes) + chunk_bytes_at<F>(e)) = out;
   } else {
     for (int64_t k = e; k < a.n; ++k) {
@@ -324,7 +319,7 @@ __global__ __launch_bounds__(256) void k_requant_scaled(RequantArgs a) {
       }
     }
     const float s = group_scale<F>(__uint_as_float(lane_umax(__float_as_uint(m), LG)));
-    const float rs = (s == 0.0f) ? 0.0f : 1.0f / s;
+    const float rs = recip_scale(s);
     if (live && li == 0) a.scale[grp] = s;
     const int64_t iters = (chunks_per_group + LG - 1) / LG;  // uniform trip count
     for (int64_t it = 0; it < iters; ++it) {
@@ -333,12 +328,9 @@ __global__ __launch_bounds__(256) void k_requant_scaled(RequantArgs a) {
       const int64_t e = (ok ? grp * a.group + c * 16 : 0);
       float h[16];
       load_floats<16>(a.h + e, h);
-      float mc = 0.0f;
-#pragma unroll
-      for (int k = 0; k < 16; ++k) mc = fmaxf(mc, __builtin_fabsf(h[k]));
       const uint64_t ge = a.entry_base + static_cast<uint64_t>(e);
       const chunk_t<F> out = quantize_any<F, R>(h, rs, chunk_thr<R, 16>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff),
-                                                chunk_has_nan<16>(h), saturates<F, R>(mc, rs));
+                                                chunk_has_nan<16>(h));
       if (ok) *reinterpret_cast<chunk_t<F>*>(static_cast<uint8_t*>(a.codes) + chunk_bytes_at<F>(e)) = out;
     }
   }

@@ -151,3 +151,32 @@ def test_int_full_size_hybrid_layer(ssmq):
         nd, ulp = code_stats("int8", cs(codes[bb:bb + 1, hh:hh + 1]).numpy(), r_codes)
         assert nd <= 1 and ulp <= 1, (tile, nd, ulp)
         assert np.array_equal(cs(scale[tile * per_tile:(tile + 1) * per_tile]).numpy(), r_scale)
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4", "e4m3"])
+def test_group_scales_over_all_binades(ssmq, fmt):
+    """Group maxima from 2^-126 to FLT_MAX (both sides of the fast division's range,
+    infinity and flushed groups): scales and codes bit-exact against the oracle. This
+    exercises the scale division and the reciprocal of every group."""
+    rng = np.random.default_rng(77)
+    group, n_groups = 16, 1 << 16
+    e = rng.integers(-126, 128, n_groups)
+    mant = rng.uniform(1.0, 2.0, n_groups)
+    mx = (mant * np.exp2(e.astype(np.float64))).astype(np.float32)
+    mx[:4] = [np.float32(3.4028235e38), np.float32(2.0 ** -112), np.float32(2.0 ** -113),
+              np.float32(1e-40)]
+    mx[4] = np.inf
+    rel = rng.uniform(-1.0, 1.0, (n_groups, group)).astype(np.float32)
+    rel[:, 0] = 1.0
+    x = (rel * mx[:, None]).astype(np.float32).ravel()
+    h = torch.from_numpy(x).to(DEV)
+    per = 2 if fmt == "int4" else 1
+    codes = torch.zeros((x.size // per,), dtype=torch.uint8, device=DEV)
+    scale = torch.zeros((n_groups,), dtype=torch.float32, device=DEV)
+    ssmq.requantize(h, codes, scale, rule="weyl", fmt=fmt, scale_group=group, step=4, layer=1,
+                    dither_block=16)
+    torch.cuda.synchronize()
+    want, wscale = oracle.requantize(fmt, "weyl", x, step=4, layer=1, block=16, group=group)
+    np.testing.assert_array_equal(scale.cpu().numpy(), wscale)
+    got = codes.cpu().numpy()
+    assert np.array_equal(got, want), np.nonzero(got != want)[0][:10]
