@@ -93,6 +93,10 @@ def lib() -> ctypes.CDLL:
                                    _i64, _i64, _i64, _int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                    _vp, _vp]
     L.orc_state_update.restype = _int
+    L.orc_state_update_fp32_grid.argtypes = [_int, _int, _u32, _u32, _u32, _u64, _u64, _i64, _i64,
+                                             _i64, _i64, _i64, _i64, _int, _vp, _vp, _vp, _vp,
+                                             _vp, _vp, _vp, _vp, _vp]
+    L.orc_state_update_fp32_grid.restype = _int
     _lib = L
     return L
 
@@ -217,6 +221,30 @@ def state_update(fmt: str, rule: str, state, scale, x, dt, A, B, C, D, *, seed=0
     if rc != 0:
         raise ValueError("oracle state_update rejected its arguments")
     return state, sc, y, hnew
+
+
+def state_update_fp32_grid(fmt: str, rule: str, state, x, dt, A, B, C, D, *, seed=0, layer=0,
+                           step=0, entry_base=0, block=16, group=0, a_per_state=None):
+    """A checkpoint write on an fp32 state: one fp32 step, then every value rounded
+    onto fmt's grid and stored as fp32. Returns (new fp32 state, group scales or
+    None, y (float64))."""
+    st = np.array(state, dtype=np.float32, copy=True, order="C")
+    batch, nheads, headdim, dstate = st.shape
+    B = _c(B, np.float32)
+    A = _c(A, np.float32)
+    if a_per_state is None:
+        a_per_state = 1 if A.ndim == 2 else 0
+    g = group if group else headdim * dstate
+    sc = np.zeros(st.size // g, np.float32) if fmt in SCALED else None
+    y = np.zeros((batch, nheads, headdim), np.float64)
+    rc = lib().orc_state_update_fp32_grid(
+        FORMATS[fmt], RULES[rule], seed & 0xFFFFFFFF, layer & 0xFFFFFFFF, step & 0xFFFFFFFF,
+        entry_base, block, group, batch, nheads, headdim, dstate, B.shape[1], a_per_state,
+        _ptr(st), _ptr(sc), _ptr(_c(x, np.float32)), _ptr(_c(dt, np.float32)), _ptr(A), _ptr(B),
+        _ptr(_c(C, np.float32)), _ptr(None if D is None else _c(D, np.float32)), _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle state_update_fp32_grid rejected its arguments")
+    return st, sc, y
 
 
 def dequantize(fmt: str, codes, scale=None, group=0) -> np.ndarray:

@@ -616,3 +616,50 @@ int orc_state_update(int f, int rule, uint32_t seed, uint32_t layer, uint32_t st
     free(hn);
     return rc;
 }
+
+/*
+ * Checkpoint write with an fp32 state (Section 5 "Periodic checkpointing";
+ * Appendix B "Decode regime", CC = 8: fp32 intermediate states, rounding at
+ * every k-th write). The state holds fp32 values. One step of eq. (rec) is
+ * taken in fp32 exactly as for the unrounded format (h_prev is the stored
+ * value), then each new value is rounded onto the grid of format f under the
+ * rule (scaled formats: group scale s as in orc_requantize) and stored back as
+ * its fp32 value: decode(code), or fl32(code value * s). The group scales are
+ * also written to `scale` when it is not NULL. Steps between checkpoints are
+ * plain fp32 steps (orc_state_update with ORC_FP32).
+ * Returns 0, or -1 on bad arguments.
+ */
+int orc_state_update_fp32_grid(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step,
+                               uint64_t entry_base, uint64_t block, int64_t group, int64_t batch,
+                               int64_t nheads, int64_t headdim, int64_t dstate, int64_t ngroups,
+                               int a_per_state, float *state, float *scale, const float *x,
+                               const float *dt, const float *A, const float *B, const float *C,
+                               const float *D, double *y) {
+    ensure_init();
+    if (f < 0 || f >= ORC_NFMT || f == ORC_FP32) return -1;
+    const int64_t n_total = batch * nheads * headdim * dstate;
+    if (is_scaled(f)) {
+        if (group == 0) group = headdim * dstate;
+        if (group <= 0 || n_total % group != 0) return -1;
+    }
+    int rc = orc_state_update(ORC_FP32, ORC_RTN, seed, layer, step, entry_base, block, 0, batch,
+                              nheads, headdim, dstate, ngroups, a_per_state, state, NULL, x, dt, A,
+                              B, C, D, y, NULL);
+    if (rc != 0) return rc;
+    const int64_t n_alloc = n_total > 0 ? n_total : 1;
+    void *codes = calloc((size_t)n_alloc, 4);
+    float *sc = is_scaled(f) ? (float *)calloc((size_t)(n_alloc / (group > 0 ? group : 1) + 1), 4)
+                             : NULL;
+    rc = orc_requantize(f, rule, seed, layer, step, entry_base, block, n_total, group, state,
+                        codes, sc);
+    if (rc == 0) {
+        for (int64_t k = 0; k < n_total; ++k) {
+            const float v = code_value(f, load_code(f, codes, k));
+            state[k] = is_scaled(f) ? v * sc[k / group] : v;
+        }
+        if (scale && sc) memcpy(scale, sc, sizeof(float) * (size_t)(n_total / group));
+    }
+    free(codes);
+    free(sc);
+    return rc;
+}
