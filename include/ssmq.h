@@ -76,6 +76,19 @@ typedef struct {
     int32_t a_per_state; /* 0: A[nheads] (Mamba-2); 1: A[nheads][dstate] (Mamba-1)        */
 } ssmq_dims;
 
+/*
+ * SSMQ_FLAG_FP32_STATE (ssmq_state_update only): a checkpoint write on an fp32
+ * state, for periodic checkpointing (Section 5 "Periodic checkpointing";
+ * Appendix B "Decode regime", CC = 8: fp32 intermediate states, rounding every
+ * k-th write). `state` holds fp32 values, read as they are; each new value is
+ * rounded onto the grid of q->format under q->rule (E4M3/INT8/INT4 with their
+ * group scale) and stored back as the fp32 value of its code (times the scale).
+ * The group scales are written to `state_scale` when it is not NULL. The steps
+ * between checkpoints are ordinary SSMQ_FP32 steps. Scale groups must be powers
+ * of two up to 1024 entries; q->format must not be SSMQ_FP32.
+ */
+enum { SSMQ_FLAG_FP32_STATE = 1 };
+
 /* How the state is written back. */
 typedef struct {
     int32_t rule;          /* ssmq_rule                                                    */
@@ -91,7 +104,7 @@ typedef struct {
     uint32_t layer;        /* l (Appendix B "Dithers"; SR key)                              */
     uint32_t step;         /* t, the integer phase counter (Section 5.4, "Computing the
                               phase in float32": an integer phase keeps every stream)      */
-    uint32_t reserved;     /* must be 0                                                    */
+    uint32_t flags;        /* 0, or SSMQ_FLAG_FP32_STATE                                    */
     uint64_t entry_base;   /* global flat index of entry 0 of this tensor, a multiple of
                               16; lets a shard reproduce the unsharded thresholds           */
 } ssmq_qparams;

@@ -32,7 +32,7 @@ class Dims(ctypes.Structure):
 class QParams(ctypes.Structure):
     _fields_ = [("rule", _i32), ("format", _i32), ("dither_block", _i32),
                 ("scale_group", _i32), ("seed", _u32), ("layer", _u32), ("step", _u32),
-                ("reserved", _u32), ("entry_base", _u64)]
+                ("flags", _u32), ("entry_base", _u64)]
 
 
 class SsmqError(RuntimeError):
@@ -95,24 +95,34 @@ def _stream(stream, ref: torch.Tensor):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+FLAG_FP32_STATE = 1
+
+
 def qparams(rule: str, fmt: str, *, dither_block=16, scale_group=0, seed=0, layer=0, step=0,
-            entry_base=0) -> QParams:
+            entry_base=0, flags=0) -> QParams:
     return QParams(RULES[rule], FORMATS[fmt], int(dither_block), int(scale_group),
-                   int(seed) & 0xFFFFFFFF, int(layer) & 0xFFFFFFFF, int(step) & 0xFFFFFFFF, 0,
-                   int(entry_base))
+                   int(seed) & 0xFFFFFFFF, int(layer) & 0xFFFFFFFF, int(step) & 0xFFFFFFFF,
+                   int(flags), int(entry_base))
 
 
 def state_update(state, scale, x, dt, A, B, C, D, y, *, rule: str, fmt: str, dither_block=16,
-                 scale_group=0, seed=0, layer=0, step=0, entry_base=0, stream=None) -> None:
+                 scale_group=0, seed=0, layer=0, step=0, entry_base=0, fp32_state=False,
+                 stream=None) -> None:
     """ssmq_state_update on [batch, nheads, headdim, dstate] state codes, in place
-    (INT4: [batch, nheads, headdim, dstate / 2] bytes)."""
+    (INT4: [batch, nheads, headdim, dstate / 2] bytes). fp32_state: a checkpoint
+    write on an fp32 state [batch, nheads, headdim, dstate] (SSMQ_FLAG_FP32_STATE)."""
     batch, nheads, headdim, dstate = state.shape
-    dstate *= ENTRIES_PER_CODE[fmt]
-    if state.element_size() != CODE_BYTES[fmt]:
-        raise ValueError(f"state element size {state.element_size()} does not match {fmt}")
+    if fp32_state:
+        if state.dtype != torch.float32:
+            raise ValueError("a checkpoint write needs an fp32 state")
+    else:
+        dstate *= ENTRIES_PER_CODE[fmt]
+        if state.element_size() != CODE_BYTES[fmt]:
+            raise ValueError(f"state element size {state.element_size()} does not match {fmt}")
     dims = Dims(batch, nheads, headdim, dstate, B.shape[1], 1 if A.dim() == 2 else 0)
     q = qparams(rule, fmt, dither_block=dither_block, scale_group=scale_group, seed=seed,
-                layer=layer, step=step, entry_base=entry_base)
+                layer=layer, step=step, entry_base=entry_base,
+                flags=FLAG_FP32_STATE if fp32_state else 0)
     _check(library().ssmq_state_update(ctypes.byref(dims), ctypes.byref(q), _ptr(state),
                                        _ptr(scale), _ptr(x), _ptr(dt), _ptr(A), _ptr(B), _ptr(C),
                                        _ptr(D), _ptr(y), _stream(stream, state)))

@@ -82,7 +82,10 @@ ssmq_status check_qparams(const ssmq_qparams* q) {
     return fail(SSMQ_EINVAL, "unknown rule %d", q->rule);
   if (q->format < SSMQ_FP16 || q->format > SSMQ_INT4)
     return fail(SSMQ_EINVAL, "unknown format %d", q->format);
-  if (q->reserved != 0) return fail(SSMQ_EINVAL, "qparams.reserved must be 0");
+  if ((q->flags & ~static_cast<uint32_t>(SSMQ_FLAG_FP32_STATE)) != 0)
+    return fail(SSMQ_EINVAL, "unknown qparams.flags bits 0x%x", q->flags);
+  if ((q->flags & SSMQ_FLAG_FP32_STATE) && q->format == SSMQ_FP32)
+    return fail(SSMQ_EINVAL, "SSMQ_FLAG_FP32_STATE rounds onto another format's grid, not FP32");
   if (!is_pow2(q->dither_block) || q->dither_block > (1 << 30))
     return fail(SSMQ_EINVAL, "dither_block %d is not a power of two in [1, 2^30]", q->dither_block);
   if (q->entry_base % 16 != 0)
@@ -134,11 +137,13 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
   if (!state || !x || !dt || !A || !B || !C || !y)
     return fail(SSMQ_EINVAL, "state, x, dt, A, B, C and y must not be NULL");
   const bool scaled = is_scaled(q->format);  // E4M3, INT8, INT4: one fp32 scale per group
-  if (scaled && !state_scale) return fail(SSMQ_EINVAL, "E4M3, INT8 and INT4 need state_scale");
+  const bool fp32_state = (q->flags & SSMQ_FLAG_FP32_STATE) != 0;
+  if (scaled && !state_scale && !fp32_state)
+    return fail(SSMQ_EINVAL, "E4M3, INT8 and INT4 need state_scale");
   if (!aligned(state, 16) || !aligned(B, 16) || !aligned(C, 16) || (d.a_per_state && !aligned(A, 16)))
     return fail(SSMQ_EALIGN, "state, B, C (and A[nheads][dstate]) must be 16-byte aligned");
   if (!aligned(x, 4) || !aligned(dt, 4) || !aligned(A, 4) || !aligned(y, 4) ||
-      (D && !aligned(D, 4)) || (scaled && !aligned(state_scale, 4)))
+      (D && !aligned(D, 4)) || (state_scale && !aligned(state_scale, 4)))
     return fail(SSMQ_EALIGN, "fp32 arrays must be 4-byte aligned");
 
   const int V = chunk_entries(q->format);
@@ -171,6 +176,10 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
   a.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block, a.toff);
   a.group_shift = scaled && is_pow2(group) ? log2i(group) : 0;
   const bool small_groups_ok = !scaled || (is_pow2(group / 16) && group / 16 <= 64);
+  a.fp32_state = fp32_state ? 1 : 0;
+  if (fp32_state && !small_groups_ok)
+    return fail(SSMQ_EUNSUPPORTED,
+                "with SSMQ_FLAG_FP32_STATE scale groups must be powers of two up to 1024 entries");
 
   // Slab kernels for per-head A: a workgroup owns whole rows of one head, two
   // 16-byte chunks per thread; with one scale per head (scaled formats) the workgroup owns
@@ -178,7 +187,7 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
   // per-workgroup scale reduction and its barriers).
   int cfg = -1;
   const int64_t head_chunks = head_size / V;
-  if (d.a_per_state == 0 && scaled && group == head_size) {
+  if (d.a_per_state == 0 && scaled && group == head_size && !fp32_state) {
     switch (head_chunks) {
       case 256: cfg = ssmq::kSlab64x4; break;
       case 512: cfg = ssmq::kSlab128x4; break;
@@ -190,7 +199,7 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
     }
     if (cfg >= 0) { a.slabs_per_head = 1; a.lanes_per_group = 0; }
   }
-  if (cfg < 0 && d.a_per_state == 0 && small_groups_ok && head_chunks % 256 == 0) {
+  if (cfg < 0 && d.a_per_state == 0 && small_groups_ok && head_chunks % 256 == 0 && !fp32_state) {
     cfg = (head_chunks % 512 == 0) ? ssmq::kSlab256x2 : ssmq::kSlab256x1;
     a.slabs_per_head = static_cast<int32_t>(
         head_chunks / (ssmq::kSlabThreads[cfg] * ssmq::kSlabChunks[cfg]));

@@ -191,7 +191,11 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
 // Row kernel: any layout whose rows are LR = dstate / V chunks; one chunk per
 // thread, chunk q = blockIdx * 256 + t.
 // ---------------------------------------------------------------------------
-template <int F, int R, bool A_PER_STATE>
+// FP32_STATE: a checkpoint write on an fp32 state. The stored values are fp32
+// (read as they are, no scale fold); each new value is rounded onto F's grid
+// and written back as the fp32 value of its code (times the group scale for
+// the scaled formats, whose scales are written only when a.scale is set).
+template <int F, int R, bool A_PER_STATE, bool FP32_STATE>
 __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   constexpr int V = Traits<F>::V;
   const int t = threadIdx.x;
@@ -206,7 +210,17 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   const int hh = static_cast<int>(bh - b * static_cast<uint32_t>(a.nheads));
   const int g = static_cast<int>(a.div_hpg.div(static_cast<uint32_t>(hh)));
   uint8_t* const state = static_cast<uint8_t*>(a.state);
-  const chunk_t<F> raw = load_stream<chunk_t<F>>(state + chunk_bytes_at<F>(e));
+  float hp[V], h[V];
+  if constexpr (FP32_STATE) {
+#pragma unroll
+    for (int i = 0; i < V / 4; ++i) {
+      const uint4 v = load_stream<uint4>(state + (e + 4 * i) * 4);
+      hp[4 * i] = __uint_as_float(v.x); hp[4 * i + 1] = __uint_as_float(v.y);
+      hp[4 * i + 2] = __uint_as_float(v.z); hp[4 * i + 3] = __uint_as_float(v.w);
+    }
+  } else {
+    decode_chunk<F>(load_stream<chunk_t<F>>(state + chunk_bytes_at<F>(e)), hp);
+  }
   const float xv = a.x[row];
   const float dtv = a.dt[bh];
   const float Dv = a.D ? a.D[hh] : 0.0f;
@@ -223,13 +237,11 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
 #pragma unroll
     for (int k = 0; k < V; ++k) dA[k] = d;
   }
-  if constexpr (Traits<F>::scaled) {  // fold the old group scale into the decay (see k_update_slab)
+  if constexpr (Traits<F>::scaled && !FP32_STATE) {  // fold the old group scale into the decay (see k_update_slab)
     const float s_old = a.scale[e >> a.group_shift];
 #pragma unroll
     for (int k = 0; k < V; ++k) dA[k] = dA[k] * s_old;
   }
-  float hp[V], h[V];
-  decode_chunk<F>(raw, hp);
   const float dx = dtv * xv;
   float ys = 0.0f;
 #pragma unroll
@@ -241,19 +253,34 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   const bool bad = !__builtin_isfinite(ys);
   ys = lane_sum(ys, a.lanes_per_row);
   if (live && cc == 0) a.y[row] = ys + Dv * xv;
-  float rs = 1.0f;
+  float rs = 1.0f, s = 1.0f;
   if constexpr (Traits<F>::scaled) {
     float m = 0.0f;
 #pragma unroll
     for (int k = 0; k < V; ++k) m = fmaxf(m, __builtin_fabsf(h[k]));
-    const float s = group_scale<F>(__uint_as_float(lane_umax(__float_as_uint(m), a.lanes_per_group)));
+    s = group_scale<F>(__uint_as_float(lane_umax(__float_as_uint(m), a.lanes_per_group)));
     rs = recip_scale(s);
-    if (live && (t & (a.lanes_per_group - 1)) == 0) a.scale[e >> a.group_shift] = s;
+    if (live && a.scale && (t & (a.lanes_per_group - 1)) == 0) a.scale[e >> a.group_shift] = s;
   }
   const uint64_t ge = a.entry_base + static_cast<uint64_t>(e);
   const chunk_t<F> out =
       quantize_any<F, R>(h, rs, chunk_thr<R, V>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff), bad);
-  if (live) store_stream(state + chunk_bytes_at<F>(e), out);
+  if constexpr (FP32_STATE) {
+    float v[V];
+    decode_chunk<F>(out, v);
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+      if constexpr (Traits<F>::scaled) v[k] = v[k] * s;
+    if (live) {
+#pragma unroll
+      for (int i = 0; i < V / 4; ++i)
+        store_stream(state + (e + 4 * i) * 4,
+                     make_uint4(__float_as_uint(v[4 * i]), __float_as_uint(v[4 * i + 1]),
+                                __float_as_uint(v[4 * i + 2]), __float_as_uint(v[4 * i + 3])));
+    }
+  } else {
+    if (live) store_stream(state + chunk_bytes_at<F>(e), out);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -378,10 +405,20 @@ static hipError_t launch_slab_cfg(const UpdateArgs& a, int cfg, hipStream_t s) {
 template <int F, int R>
 static hipError_t launch_rows(const UpdateArgs& a, bool a_per_state, hipStream_t s) {
   const unsigned grid = static_cast<unsigned>((a.n_chunks + 255) / 256);
-  if (a_per_state)
-    hipLaunchKernelGGL((k_update_rows<F, R, true>), dim3(grid), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_update_rows<F, R, false>), dim3(grid), dim3(256), 0, s, a);
+  if (a.fp32_state) {
+    if constexpr (F != kFP32) {
+      if (a_per_state)
+        hipLaunchKernelGGL((k_update_rows<F, R, true, true>), dim3(grid), dim3(256), 0, s, a);
+      else
+        hipLaunchKernelGGL((k_update_rows<F, R, false, true>), dim3(grid), dim3(256), 0, s, a);
+    } else {
+      return hipErrorInvalidValue;
+    }
+  } else if (a_per_state) {
+    hipLaunchKernelGGL((k_update_rows<F, R, true, false>), dim3(grid), dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((k_update_rows<F, R, false, false>), dim3(grid), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

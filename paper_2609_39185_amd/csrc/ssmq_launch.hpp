@@ -70,6 +70,7 @@ struct UpdateArgs {
   int64_t head_size;        // headdim * dstate
   int64_t n_chunks;         // total entries / V
   uint64_t entry_base;
+  int32_t fp32_state;       // row kernel: fp32 state, values rounded onto F's grid (a checkpoint)
   Thr thr;
   uint32_t toff[16];        // threshold offset of entry k of a chunk
   uint32_t pass_thr_inc;    // slab kernels: threshold base increment per pass ...

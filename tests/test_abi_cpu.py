@@ -60,8 +60,13 @@ def test_state_update_validation(lib):
     assert _update(lib, good, q) == EINVAL
     q = Q("weyl", "bf16"); q.format = 9
     assert _update(lib, good, q) == EINVAL
-    q = Q("weyl", "bf16"); q.reserved = 1
-    assert _update(lib, good, q) == EINVAL
+    q = Q("weyl", "bf16"); q.flags = 2
+    assert _update(lib, good, q) == EINVAL                            # unknown flag
+    q = Q("weyl", "fp32", flags=lib.FLAG_FP32_STATE)
+    assert _update(lib, good, q) == EINVAL                            # fp32 onto fp32
+    q = Q("weyl", "int8", flags=lib.FLAG_FP32_STATE)                   # whole-head groups
+    assert _update(lib, good, q) == EUNSUPPORTED
+    assert _update(lib, good, Q("philox", "int8")) == EINVAL           # INT8 needs its scale
     assert _update(lib, good, Q("weyl", "bf16", dither_block=24)) == EINVAL
     assert _update(lib, good, Q("weyl", "bf16", entry_base=8)) == EINVAL
     assert _update(lib, D(1, 4, 64, 128, 3, 0), Q("weyl", "bf16")) == EINVAL
