@@ -41,6 +41,12 @@ def parse_args():
     ap.add_argument("--state-error", action="store_true",
                     help="instead of throughput: quantized states vs an FP32 twin in lockstep")
     ap.add_argument("--block", type=int, default=512, help="--state-error: steps per reported block")
+    ap.add_argument("--se-format", default="fp16", help="--state-error: storage format")
+    ap.add_argument("--se-group", type=int, default=16, help="--state-error: entries per scale")
+    ap.add_argument("--se-memory", default="short", choices=("short", "trained"),
+                    help="--state-error: decay-rate recipe")
+    ap.add_argument("--se-cc", type=int, default=0,
+                    help="--state-error: also run checkpointed rules, rounding every k-th write")
     ap.add_argument("--variants", default="bf16:weyl,bf16:sr,bf16:rtn,bf16:philox,"
                                           "e4m3:weyl,e4m3:sr,e4m3:rtn,e4m3:philox,"
                                           "int8:weyl,int8:sr,int8:rtn,int8:philox,"
@@ -95,7 +101,8 @@ def main() -> int:
     w = wl.WORKLOADS[args.workload]
     if args.state_error:
         res = state_error_study(w, steps=args.steps or w.steps, layers=args.layers or w.layers,
-                                block=args.block, device=dev)
+                                block=args.block, device=dev, fmt=args.se_format,
+                                group=args.se_group, memory=args.se_memory, cc=args.se_cc)
         print(json.dumps(res), flush=True)
         return 0
     if args.steps is None:
@@ -252,8 +259,30 @@ def mean_step_size() -> float:
     return float(np.trapezoid(np.logaddexp(0.0, z - 4.0) * pdf, z))
 
 
+def decode_state(fmt: str, codes, scale, group: int):
+    """fp32 values of a stored state on the GPU (torch), for the error metric only:
+    fp16/bf16 reinterpret, E4M3 and INT8/INT4 times their group scale."""
+    import torch
+
+    if fmt == "fp32":
+        return codes.view(torch.float32)
+    if fmt in ("fp16", "bf16"):
+        return codes.view({"fp16": torch.float16, "bf16": torch.bfloat16}[fmt]).float()
+    if fmt == "e4m3":
+        v = codes.view(torch.float8_e4m3fn).float()
+    elif fmt == "int8":
+        v = codes.view(torch.int8).float()
+    else:  # int4: even entry in the low nibble
+        lo = (codes & 0xF).to(torch.int16)
+        hi = (codes >> 4).to(torch.int16)
+        v = torch.stack(((lo ^ 8) - 8, (hi ^ 8) - 8), dim=-1).flatten(-2).float()
+    flat = v.reshape(-1, group) * scale.reshape(-1, 1)
+    return flat.reshape(v.shape)
+
+
 def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: str = "fp16",
-                      rules=SE_RULES, on_step=None, init=None) -> dict:
+                      group: int = 16, memory: str = "short", cc: int = 0, rules=SE_RULES,
+                      on_step=None, init=None) -> dict:
     """Quantized states against an unrounded FP32 twin, decoded in lockstep on the
     same teacher-forced inputs (Appendix B, "Open-loop replay" and "Decode regime").
 
@@ -263,10 +292,17 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
     batch and steps; the model-level figure is the mean over layers. Errors are also
     split into memory bins by tau = 1 / (1 - exp(A * E[dt])).
 
-    Inputs: A, D per layer as in the throughput bench; x, dt, B, C for all layers of
-    step t from one generator seeded with splitmix64(4000, t). on_step(t, x, dt, B, C)
-    is called with each step's inputs, and init = {"A", "D", "codes0"} replaces the
-    generated layer parameters and initial codes (both for cross-checks on small sizes).
+    fmt: fp16, bf16, e4m3, int8 or int4 (the scaled ones with `group` entries per
+    scale). memory: "short" (the throughput bench's decay rates) or "trained" (a
+    trained model's spread, workloads.layer_params_trained_memory). cc > 0 adds,
+    for RTN, SR (seed 0) and Weyl, a periodically checkpointed run: an fp32 state
+    rounded onto the format's grid at every cc-th write only (Section 5 "Periodic
+    checkpointing").
+
+    Inputs: A, D per layer; x, dt, B, C for all layers of step t from one generator
+    seeded with splitmix64(4000, t). on_step(t, x, dt, B, C) is called with each
+    step's inputs, and init = {"A", "D", "codes0"} replaces the generated layer
+    parameters and initial codes (both for cross-checks on small sizes).
     """
     import numpy as np
     import torch
@@ -278,27 +314,47 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
         raise ValueError("the state-error study is defined on the Mamba-1 shapes")
     b, d, N = w.batch, w.nheads, w.dstate
     L = layers
+    scaled = fmt in ("e4m3", "int8", "int4")
+    g_ = group if scaled else 0
     n_blocks = (steps + block - 1) // block
     code_dt = wl.CODE_TORCH_DTYPE[fmt]
-    val_dt = {"fp16": torch.float16, "bf16": torch.bfloat16}[fmt]
+    per = 2 if fmt == "int4" else 1
+    params = wl.layer_params if memory == "short" else wl.layer_params_trained_memory
     A, D = [], []
     for ell in range(L):
         if init is not None:
             a, dd = init["A"][ell].to(device), init["D"][ell].to(device)
         else:
-            a, dd = wl.layer_params(w.family, d, N, seed=1000 + ell, device=device)
+            a, dd = params(w.family, d, N, seed=1000 + ell, device=device)
         A.append(a.contiguous())
         D.append(dd.contiguous())
-    codes = {r: torch.empty((L, b, d, 1, N), dtype=code_dt, device=device) for r in rules}
+    runs = list(rules) + ([(r, sd, cc) for r, sd in (("rtn", 0), ("sr", 0), ("weyl", 0))]
+                          if cc > 0 else [])
+    codes, scales = {}, {}
+    for r in runs:
+        if len(r) == 3:
+            codes[r] = torch.empty((L, b, d, 1, N), dtype=torch.float32, device=device)
+        else:
+            codes[r] = torch.empty((L, b, d, 1, N // per), dtype=code_dt, device=device)
+            scales[r] = (torch.empty((L, b * d * N // g_), dtype=torch.float32, device=device)
+                         if scaled else None)
     twin = torch.empty((L, b, d, 1, N), dtype=torch.float32, device=device)
     for ell in range(L):
         if init is not None:
-            c0 = init["codes0"][ell].to(device)
+            c0, s0 = init["codes0"][ell].to(device), None
+            if scaled:
+                s0 = init["scale0"][ell].to(device)
         else:
-            c0, _ = wl.initial_state(fmt, b, d, 1, N, seed=3000 + ell, device=device)
-        for r in rules:
-            codes[r][ell].copy_(c0)
-        twin[ell].copy_(c0.view(val_dt).float())
+            c0, s0 = wl.initial_state(fmt, b, d, 1, N, seed=3000 + ell, group=g_, device=device)
+        h0 = decode_state(fmt, c0, s0, g_ or 1)
+        for r in runs:
+            if len(r) == 3:
+                codes[r][ell].copy_(h0)
+            else:
+                codes[r][ell].copy_(c0)
+                if scaled:
+                    scales[r][ell].copy_(s0)
+        twin[ell].copy_(h0)
     twin_codes = twin.view(torch.int32)
     y = torch.empty((b, d, 1), dtype=torch.float32, device=device)
 
@@ -310,39 +366,54 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
     n_bins = len(TAU_EDGES) + 1
     onehot = torch.nn.functional.one_hot(bins, n_bins).to(torch.float64)  # [L, d, N, n_bins]
 
-    num = {r: torch.zeros((n_blocks, L, n_bins), dtype=torch.float64, device=device) for r in rules}
+    num = {r: torch.zeros((n_blocks, L, n_bins), dtype=torch.float64, device=device) for r in runs}
     den = torch.zeros((n_blocks, L, n_bins), dtype=torch.float64, device=device)
     # per-entry sums over batch and the steps of the current block
-    acc = {r: torch.zeros((L, d, N), dtype=torch.float64, device=device) for r in rules}
+    acc = {r: torch.zeros((L, d, N), dtype=torch.float64, device=device) for r in runs}
     acc_h = torch.zeros((L, d, N), dtype=torch.float64, device=device)
     stream = torch.cuda.current_stream(device)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for t in range(1, steps + 1):
-        g = torch.Generator(device=device)
-        g.manual_seed(wl.splitmix64(4000, t))
-        x = torch.randn((L, b, d, 1), generator=g, device=device)
-        dt = torch.nn.functional.softplus(torch.randn((L, b, d), generator=g, device=device) - 4.0)
-        B = torch.randn((L, b, 1, N), generator=g, device=device)
-        C = torch.randn((L, b, 1, N), generator=g, device=device)
+        gen = torch.Generator(device=device)
+        gen.manual_seed(wl.splitmix64(4000, t))
+        x = torch.randn((L, b, d, 1), generator=gen, device=device)
+        dt = torch.nn.functional.softplus(torch.randn((L, b, d), generator=gen, device=device) - 4.0)
+        B = torch.randn((L, b, 1, N), generator=gen, device=device)
+        C = torch.randn((L, b, 1, N), generator=gen, device=device)
         if on_step is not None:
             on_step(t, x, dt, B, C)
         for ell in range(L):
             args = (x[ell], dt[ell], A[ell], B[ell], C[ell], D[ell], y)
             ssmq.state_update(twin_codes[ell], None, *args, rule="rtn", fmt="fp32",
                               dither_block=w.dither_block, layer=ell, step=t, stream=stream)
-            for r in rules:
-                ssmq.state_update(codes[r][ell], None, *args, rule=r[0], fmt=fmt, seed=r[1],
-                                  dither_block=w.dither_block, layer=ell, step=t, stream=stream)
+            for r in runs:
+                if len(r) == 3:
+                    if t % r[2] == 0:
+                        ssmq.state_update(codes[r][ell], None, *args, rule=r[0], fmt=fmt,
+                                          seed=r[1], scale_group=g_, dither_block=w.dither_block,
+                                          layer=ell, step=t, fp32_state=True, stream=stream)
+                    else:
+                        ssmq.state_update(codes[r][ell].view(torch.int32), None, *args,
+                                          rule="rtn", fmt="fp32", dither_block=w.dither_block,
+                                          layer=ell, step=t, stream=stream)
+                else:
+                    ssmq.state_update(codes[r][ell], None if scales[r] is None else scales[r][ell],
+                                      *args, rule=r[0], fmt=fmt, seed=r[1], scale_group=g_,
+                                      dither_block=w.dither_block, layer=ell, step=t,
+                                      stream=stream)
         acc_h += twin.square().sum(dim=(1, 3))
-        for r in rules:
-            e = codes[r].view(val_dt).float().sub_(twin)
+        for r in runs:
+            if len(r) == 3:
+                e = codes[r] - twin
+            else:
+                e = decode_state(fmt, codes[r], scales[r], g_ or 1).sub_(twin)
             acc[r] += e.square_().sum(dim=(1, 3))
         if t % block == 0 or t == steps:
             k = (t - 1) // block
             den[k] = torch.einsum("ldn,ldnk->lk", acc_h, onehot)
             acc_h.zero_()
-            for r in rules:
+            for r in runs:
                 num[r][k] = torch.einsum("ldn,ldnk->lk", acc[r], onehot)
                 acc[r].zero_()
             print(f"state-error study: {t} of {steps} steps, "
@@ -351,10 +422,11 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
     elapsed = time.perf_counter() - t_start
 
     def name(r):
-        return r[0] if r[0] != "sr" else f"sr_seed{r[1]}"
+        base = r[0] if r[0] != "sr" else f"sr_seed{r[1]}"
+        return base if len(r) == 2 else f"{base}_cc{r[2]}"
 
     out_rules, out_bins = {}, {}
-    for r in rules:
+    for r in runs:
         tot = num[r].sum(-1) / den.sum(-1)                                   # [blocks, L]
         out_rules[name(r)] = [float(v) for v in tot.mean(-1)]
         per_bin = num[r] / den                                               # [blocks, L, bins]
@@ -368,7 +440,8 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
     return {
         "study": "state_error",
         "metric": "relative state error sum((h_hat-h)^2)/sum(h^2) per block, mean over layers",
-        "workload": w.name, "format": fmt, "batch": b, "d_inner": d, "dstate": N, "layers": L,
+        "workload": w.name, "format": fmt, "scale_group": g_ or None, "memory": memory,
+        "checkpoint_every": cc or None, "batch": b, "d_inner": d, "dstate": N, "layers": L,
         "steps": steps, "block": block, "dither_block": w.dither_block, "data": "synthetic",
         "mean_dt": dt_mean, "tau_bin_share": dict(zip(("<10", "10-100", "100-1000", ">=1000"), share)),
         "error": out_rules,
@@ -377,7 +450,7 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
         "error_by_tau_bin": out_bins,
         "wall_s": elapsed,
         "ms_per_step": 1e3 * elapsed / steps,
-        "launches_per_step": L * (1 + len(rules)),
+        "launches_per_step": L * (1 + len(runs)),
     }
 
 

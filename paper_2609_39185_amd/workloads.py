@@ -102,6 +102,22 @@ def layer_params(family: str, nheads: int, dstate: int, seed: int, device="cpu")
     return A.contiguous(), D.contiguous()
 
 
+def layer_params_trained_memory(family: str, nheads: int, dstate: int, seed: int, device="cpu"):
+    """A and D with a trained model's spread of memories: with E[dt] = 0.029, 80 % of
+    the decay rates give tau = 1 / (1 - exp(A E[dt])) below about 35 steps
+    (A = -exp(U[0, 2.5])) and 20 % give tau from about 100 to 1900 steps
+    (A = -exp(U[-4, -1.1])), close to the 13-23 % with tau >= 100 and up to 5 %
+    with tau >= 1000 measured on trained models (Section 2)."""
+    g = _gen(splitmix64(seed, 4), device)
+    shape = (nheads, dstate) if family == "mamba1" else (nheads,)
+    short = torch.rand(shape, generator=g, device=device, dtype=torch.float32) * 2.5
+    long_ = torch.rand(shape, generator=g, device=device, dtype=torch.float32) * 2.9 - 4.0
+    pick = torch.rand(shape, generator=g, device=device, dtype=torch.float32) < 0.2
+    A = -torch.exp(torch.where(pick, long_, short))
+    D = torch.randn((nheads,), generator=g, device=device, dtype=torch.float32)
+    return A.contiguous(), D.contiguous()
+
+
 def step_inputs(batch: int, nheads: int, headdim: int, dstate: int, ngroups: int, seed: int,
                 device="cpu"):
     """x, dt, B, C of one (layer, step)."""

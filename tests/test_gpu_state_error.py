@@ -41,13 +41,22 @@ def _small(batch, d, layers, steps):
                                steps=steps)
 
 
-def _oracle_replay(w, L, steps, block, init, inputs, rules):
+def _oracle_replay(w, L, steps, block, init, inputs, rules, fmt="fp16", group=16, cc=0):
+    """The study redone by the oracle on the same inputs; returns {run: errors per block}."""
     b, d, N = w.batch, w.nheads, w.dstate
-    codes = {r: [wl.to_numpy_codes("fp16", init["codes0"][ell]) for ell in range(L)] for r in rules}
-    twin = [oracle.dequantize("fp16", c).reshape(b, d, 1, N).view(np.uint32).copy()
-            for c in codes[rules[0]]]
+    scaled = fmt in oracle.SCALED
+    g = group if scaled else 0
+    runs = list(rules) + ([(r, sd, cc) for r, sd in (("rtn", 0), ("sr", 0), ("weyl", 0))]
+                          if cc > 0 else [])
+    codes0 = [wl.to_numpy_codes(fmt, init["codes0"][ell]) for ell in range(L)]
+    scale0 = [init["scale0"][ell].numpy() if scaled else None for ell in range(L)]
+    h0 = [oracle.dequantize(fmt, codes0[ell], scale0[ell], g).reshape(b, d, 1, N)
+          for ell in range(L)]
+    st = {r: [(h0[ell].copy() if len(r) == 3 else (codes0[ell].copy(), None if scale0[ell] is None
+               else scale0[ell].copy())) for ell in range(L)] for r in runs}
+    twin = [h.view(np.uint32).copy() for h in h0]
     n_blocks = (steps + block - 1) // block
-    num = {r: np.zeros((n_blocks, L)) for r in rules}
+    num = {r: np.zeros((n_blocks, L)) for r in runs}
     den = np.zeros((n_blocks, L))
     for t, x, dt, B, C in inputs:
         k = (t - 1) // block
@@ -57,13 +66,32 @@ def _oracle_replay(w, L, steps, block, init, inputs, rules):
                                                      step=t, block=w.dither_block)
             h = twin[ell].view(np.float32).astype(np.float64)
             den[k, ell] += np.sum(h * h)
-            for r in rules:
-                codes[r][ell], _, _, _ = oracle.state_update("fp16", r[0], codes[r][ell], None, *args,
-                                                             seed=r[1], layer=ell, step=t,
-                                                             block=w.dither_block)
-                e = oracle.decode("fp16", codes[r][ell]).reshape(h.shape) - h
-                num[r][k, ell] += np.sum(e * e)
-    return {r: (num[r] / den).mean(-1) for r in rules}
+            for r in runs:
+                if len(r) == 3:
+                    if t % r[2] == 0:
+                        v, _, _ = oracle.state_update_fp32_grid(fmt, r[0], st[r][ell], *args,
+                                                                seed=r[1], layer=ell, step=t,
+                                                                block=w.dither_block, group=g)
+                    else:
+                        v, _, _, _ = oracle.state_update("fp32", "rtn", st[r][ell].view(np.uint32),
+                                                         None, *args, layer=ell, step=t,
+                                                         block=w.dither_block)
+                        v = v.view(np.float32)
+                    st[r][ell] = v
+                    val = v.astype(np.float64)
+                else:
+                    c, sc = st[r][ell]
+                    c, sc, _, _ = oracle.state_update(fmt, r[0], c, sc, *args, seed=r[1], layer=ell,
+                                                      step=t, block=w.dither_block, group=g)
+                    st[r][ell] = (c, sc)
+                    val = oracle.dequantize(fmt, c, sc, g).reshape(h.shape).astype(np.float64)
+                num[r][k, ell] += np.sum((val - h) ** 2)
+    return {r: (num[r] / den).mean(-1) for r in runs}
+
+
+def _name(r):
+    base = r[0] if r[0] != "sr" else f"sr_seed{r[1]}"
+    return base if len(r) == 2 else f"{base}_cc{r[2]}"
 
 
 def test_study_matches_oracle_replay():
@@ -87,10 +115,37 @@ def test_study_matches_oracle_replay():
     _say("oracle replay of the same inputs")
     ref = _oracle_replay(w, L, steps, block, init, inputs, bench.SE_RULES)
     for r in bench.SE_RULES:
-        name = r[0] if r[0] != "sr" else f"sr_seed{r[1]}"
-        got = np.array(res["error"][name])
-        _say(f"  {name}: gpu {got} oracle {ref[r]}")
+        got = np.array(res["error"][_name(r)])
+        _say(f"  {_name(r)}: gpu {got} oracle {ref[r]}")
         np.testing.assert_allclose(got, ref[r], rtol=1e-3)
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4", "e4m3"])
+def test_scaled_study_with_checkpoints_matches_oracle_replay(fmt):
+    """Block-16 scaled formats, the trained-memory decays and CC = 4 checkpoints."""
+    L, steps, block = 1, 24, 8
+    w = _small(2, 64, L, steps)
+    b, d, N = w.batch, w.nheads, w.dstate
+    init = {"A": [], "D": [], "codes0": [], "scale0": []}
+    for ell in range(L):
+        a, dd = wl.layer_params_trained_memory("mamba1", d, N, seed=150 + ell)
+        c0, s0 = wl.initial_state(fmt, b, d, 1, N, seed=160 + ell, group=16)
+        init["A"].append(a)
+        init["D"].append(dd)
+        init["codes0"].append(c0)
+        init["scale0"].append(s0)
+    inputs = []
+
+    def keep(t, x, dt, B, C):
+        inputs.append((t, x.cpu().numpy(), dt.cpu().numpy(), B.cpu().numpy(), C.cpu().numpy()))
+
+    res = bench.state_error_study(w, steps=steps, layers=L, block=block, device=DEV, fmt=fmt,
+                                  group=16, memory="trained", cc=4, on_step=keep, init=init)
+    ref = _oracle_replay(w, L, steps, block, init, inputs, bench.SE_RULES, fmt=fmt, group=16, cc=4)
+    for r, want in ref.items():
+        got = np.array(res["error"][_name(r)])
+        _say(f"  {fmt} {_name(r)}: gpu {got} oracle {want}")
+        np.testing.assert_allclose(got, want, rtol=2e-3)
 
 
 def test_errors_follow_the_per_write_noise_lemma():
