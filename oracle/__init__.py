@@ -97,6 +97,12 @@ def lib() -> ctypes.CDLL:
                                              _i64, _i64, _i64, _i64, _int, _vp, _vp, _vp, _vp,
                                              _vp, _vp, _vp, _vp, _vp]
     L.orc_state_update_fp32_grid.restype = _int
+    L.orc_state_update_ex.argtypes = [_int, _int, _u32, _u32, _u32, _u64, _u64, _i64, _i64, _i64,
+                                      _i64, _i64, _i64, _int, _vp, _vp, _vp, _vp, _vp, _int, _vp,
+                                      _vp, _vp, _vp, _vp, _vp, _vp]
+    L.orc_state_update_ex.restype = _int
+    L.orc_conv1d_update.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, _vp, _int, _vp]
+    L.orc_conv1d_update.restype = _int
     _lib = L
     return L
 
@@ -191,8 +197,11 @@ def requantize(fmt: str, rule: str, h, *, seed=0, layer=0, step=0, entry_base=0,
 
 
 def state_update(fmt: str, rule: str, state, scale, x, dt, A, B, C, D, *, seed=0, layer=0,
-                 step=0, entry_base=0, block=16, group=0, a_per_state=None):
+                 step=0, entry_base=0, block=16, group=0, a_per_state=None, dt_bias=None,
+                 dt_softplus=False, z=None):
     """One fused step. state has shape [batch, nheads, headdim, dstate] (codes).
+    dt_bias / dt_softplus / z: the decode-step operations around the update
+    (dt' = softplus(dt + dt_bias), y' = y * silu(z)).
 
     Returns (new_state, new_scale, y (float64), h_new (fp32 pre-rounding)).
     """
@@ -213,11 +222,14 @@ def state_update(fmt: str, rule: str, state, scale, x, dt, A, B, C, D, *, seed=0
     D = None if D is None else _c(D, np.float32)
     y = np.zeros((batch, nheads, headdim), np.float64)
     hnew = np.zeros((batch, nheads, headdim, dstate), np.float32)
-    rc = lib().orc_state_update(FORMATS[fmt], RULES[rule], seed & 0xFFFFFFFF, layer & 0xFFFFFFFF,
-                                step & 0xFFFFFFFF, entry_base, block, group, batch, nheads,
-                                headdim, dstate, ngroups, a_per_state, _ptr(state), _ptr(sc),
-                                _ptr(x), _ptr(dt), _ptr(A), _ptr(B), _ptr(C), _ptr(D), _ptr(y),
-                                _ptr(hnew))
+    bias = None if dt_bias is None else _c(dt_bias, np.float32)
+    zz = None if z is None else _c(z, np.float32)
+    rc = lib().orc_state_update_ex(FORMATS[fmt], RULES[rule], seed & 0xFFFFFFFF,
+                                   layer & 0xFFFFFFFF, step & 0xFFFFFFFF, entry_base, block, group,
+                                   batch, nheads, headdim, dstate, ngroups, a_per_state,
+                                   _ptr(state), _ptr(sc), _ptr(x), _ptr(dt), _ptr(bias),
+                                   1 if dt_softplus else 0, _ptr(zz), _ptr(A), _ptr(B), _ptr(C),
+                                   _ptr(D), _ptr(y), _ptr(hnew))
     if rc != 0:
         raise ValueError("oracle state_update rejected its arguments")
     return state, sc, y, hnew
@@ -245,6 +257,21 @@ def state_update_fp32_grid(fmt: str, rule: str, state, x, dt, A, B, C, D, *, see
     if rc != 0:
         raise ValueError("oracle state_update_fp32_grid rejected its arguments")
     return st, sc, y
+
+
+def conv1d_update(state, x, weight, bias=None, act=True):
+    """Causal depthwise conv1d decode update: state [batch, channels, width] shifts
+    and takes x [batch, channels]; returns (new state, out (float64))."""
+    st = np.array(state, dtype=np.float32, copy=True, order="C")
+    batch, channels, width = st.shape
+    out = np.zeros((batch, channels), np.float64)
+    rc = lib().orc_conv1d_update(batch, channels, width, _ptr(st), _ptr(_c(x, np.float32)),
+                                 _ptr(_c(weight, np.float32)),
+                                 _ptr(None if bias is None else _c(bias, np.float32)),
+                                 1 if act else 0, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle conv1d_update rejected its arguments")
+    return st, out
 
 
 def dequantize(fmt: str, codes, scale=None, group=0) -> np.ndarray:

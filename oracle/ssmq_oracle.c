@@ -558,12 +558,54 @@ int orc_requantize(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step
  * under (rule, format) with the thresholds of global entry entry_base + flat index.
  * Returns 0, or -1 on bad arguments.
  */
+/*
+ * The decode-step operations on either side of the update, as in the Mamba
+ * reference implementation the paper's runners follow (Appendix B "Runners":
+ * "conv and gating exactly as in the reference"):
+ *   step size   dt' = softplus(fl32(dt + dt_bias)), softplus(v) = log(1 + e^v)
+ *               evaluated in double and rounded once (v itself above 20, where
+ *               the two agree in fp32);
+ *   gate        y' = y * silu(z), silu(z) = z / (1 + e^-z), in double;
+ *   conv1d      the causal depthwise convolution's state shifts by one position
+ *               and takes the new input; out = sum_i state_i w_i + bias, in
+ *               double, optionally through silu.
+ */
+static float softplus_dt(float v) {
+    if (v > 20.0f) return v;
+    return (float)log1p(exp((double)v));
+}
+
+static double silu(double z) { return z / (1.0 + exp(-z)); }
+
+int orc_state_update_ex(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step,
+                        uint64_t entry_base, uint64_t block, int64_t group, int64_t batch,
+                        int64_t nheads, int64_t headdim, int64_t dstate, int64_t ngroups,
+                        int a_per_state, void *state, float *scale, const float *x,
+                        const float *dt, const float *dt_bias, int dt_softplus, const float *z,
+                        const float *A, const float *B, const float *C, const float *D, double *y,
+                        float *hnew);
+
 int orc_state_update(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step,
                      uint64_t entry_base, uint64_t block, int64_t group, int64_t batch,
                      int64_t nheads, int64_t headdim, int64_t dstate, int64_t ngroups,
                      int a_per_state, void *state, float *scale, const float *x, const float *dt,
                      const float *A, const float *B, const float *C, const float *D, double *y,
                      float *hnew) {
+    return orc_state_update_ex(f, rule, seed, layer, step, entry_base, block, group, batch, nheads,
+                               headdim, dstate, ngroups, a_per_state, state, scale, x, dt, NULL, 0,
+                               NULL, A, B, C, D, y, hnew);
+}
+
+/* As orc_state_update, with dt' = (softplus if dt_softplus)(dt + dt_bias) per
+ * (batch, head) (dt_bias [nheads] or NULL) and y gated by silu(z) (z shaped as
+ * y, or NULL). */
+int orc_state_update_ex(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step,
+                        uint64_t entry_base, uint64_t block, int64_t group, int64_t batch,
+                        int64_t nheads, int64_t headdim, int64_t dstate, int64_t ngroups,
+                        int a_per_state, void *state, float *scale, const float *x,
+                        const float *dt, const float *dt_bias, int dt_softplus, const float *z,
+                        const float *A, const float *B, const float *C, const float *D, double *y,
+                        float *hnew) {
     ensure_init();
     if (f < 0 || f >= ORC_NFMT || batch < 0 || nheads <= 0 || headdim <= 0 || dstate <= 0 ||
         ngroups <= 0 || nheads % ngroups != 0 || block == 0)
@@ -580,7 +622,9 @@ int orc_state_update(int f, int rule, uint32_t seed, uint32_t layer, uint32_t st
     for (int64_t b = 0; b < batch; ++b) {
         for (int64_t hd = 0; hd < nheads; ++hd) {
             const int64_t g = hd / heads_per_group;
-            const float dtv = dt[b * nheads + hd];
+            float dtv = dt[b * nheads + hd];
+            if (dt_bias) dtv = dtv + dt_bias[hd];
+            if (dt_softplus) dtv = softplus_dt(dtv);
             const float *Bg = B + (b * ngroups + g) * dstate;
             const float *Cg = C + (b * ngroups + g) * dstate;
             const float Dv = D ? D[hd] : 0.0f;
@@ -607,6 +651,7 @@ int orc_state_update(int f, int rule, uint32_t seed, uint32_t layer, uint32_t st
                     acc += (double)Cg[n] * (double)h_new;
                 }
                 y[row] = acc + (double)Dv * (double)xv;
+                if (z) y[row] *= silu((double)z[row]);
             }
         }
     }
@@ -662,4 +707,28 @@ int orc_state_update_fp32_grid(int f, int rule, uint32_t seed, uint32_t layer, u
     free(codes);
     free(sc);
     return rc;
+}
+
+/*
+ * Causal depthwise conv1d decode update (the reference's convolution state):
+ * state [batch][channels][width] holds the last `width` inputs of each channel,
+ * oldest first. The state shifts by one and takes x [batch][channels]; then
+ * out[b][c] = sum_i state[b][c][i] * weight[c][i] + bias[c] (bias may be NULL),
+ * accumulated in double, and passed through silu when `act` is 1.
+ */
+int orc_conv1d_update(int64_t batch, int64_t channels, int64_t width, float *state,
+                      const float *x, const float *weight, const float *bias, int act,
+                      double *out) {
+    if (batch < 0 || channels <= 0 || width <= 0) return -1;
+    for (int64_t b = 0; b < batch; ++b) {
+        for (int64_t c = 0; c < channels; ++c) {
+            float *s = state + (b * channels + c) * width;
+            for (int64_t i = 0; i + 1 < width; ++i) s[i] = s[i + 1];
+            s[width - 1] = x[b * channels + c];
+            double acc = bias ? (double)bias[c] : 0.0;
+            for (int64_t i = 0; i < width; ++i) acc += (double)s[i] * (double)weight[c * width + i];
+            out[b * channels + c] = act ? silu(acc) : acc;
+        }
+    }
+    return 0;
 }
