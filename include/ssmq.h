@@ -148,6 +148,49 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
                               float* y, void* stream);
 
 /*
+ * The decode-step operations on either side of the update, fused into it
+ * (Appendix B "Runners": conv and gating as in the Mamba reference):
+ *   dt' = dt + dt_bias[head]                   (dt_bias non-NULL)
+ *   dt' = softplus(dt') = log(1 + exp(dt'))    (dt_softplus = 1; evaluated in
+ *         double and rounded once; values above 20 are kept as they are)
+ *   y'  = y * silu(z) = y * z / (1 + exp(-z))  (z non-NULL, shaped as y)
+ * The update then uses dt' in place of dt. The group-wise RMS normalization of
+ * Mamba-2 spans heads and stays outside.
+ */
+typedef struct {
+    const float* dt_bias;  /* [nheads] fp32 device pointer, or NULL [4 B]        */
+    int32_t dt_softplus;   /* 0 or 1                                              */
+    int32_t reserved;      /* must be 0                                           */
+    const float* z;        /* [batch][nheads][headdim] fp32, or NULL [4 B]        */
+} ssmq_step_opts;
+
+/*
+ * ssmq_state_update_ex -- ssmq_state_update with the decode-step options above
+ * (opts may be NULL: then it is ssmq_state_update). Same arguments, layouts,
+ * requirements and errors; opts pointers are device pointers.
+ */
+ssmq_status ssmq_state_update_ex(const ssmq_dims* dims, const ssmq_qparams* q,
+                                 const ssmq_step_opts* opts, void* state, float* state_scale,
+                                 const float* x, const float* dt, const float* A, const float* B,
+                                 const float* C, const float* D, float* y, void* stream);
+
+/*
+ * ssmq_conv1d_update -- the causal depthwise convolution's decode step (the
+ * Mamba reference's convolution state; Appendix B "Runners").
+ *   conv_state [batch][channels][width] fp32, the last `width` inputs of each
+ *              channel, oldest first; shifted by one and x appended, in place
+ *   x          [batch][channels] fp32, the new input
+ *   weight     [channels][width] fp32; bias [channels] fp32 or NULL
+ *   out        [batch][channels] fp32: bias + sum_k state[k] weight[k], through
+ *              silu when act = 1 (accumulated in fp32 by FMA, k ascending)
+ * All device pointers, 4-byte aligned; 1 <= width <= 64; batch * channels < 2^32.
+ * For Mamba-2 the channels are x, B and C side by side (d_inner + 2 ngroups dstate).
+ */
+ssmq_status ssmq_conv1d_update(int64_t batch, int32_t channels, int32_t width, float* conv_state,
+                               const float* x, const float* weight, const float* bias,
+                               int32_t act, float* out, void* stream);
+
+/*
  * ssmq_requantize -- write fp32 values into a storage format under a rule.
  *
  * The rounding step alone (Section 2, eq. (dither); Appendix B "Formats"):

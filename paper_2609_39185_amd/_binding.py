@@ -35,14 +35,18 @@ class QParams(ctypes.Structure):
                 ("flags", _u32), ("entry_base", _u64)]
 
 
+class StepOpts(ctypes.Structure):
+    _fields_ = [("dt_bias", _vp), ("dt_softplus", _i32), ("reserved", _i32), ("z", _vp)]
+
+
 class SsmqError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"ssmq status {status}: {message}")
         self.status = status
 
 
-EXPORTS = ("ssmq_state_update", "ssmq_requantize", "ssmq_dither_fill", "ssmq_status_string",
-           "ssmq_last_error")
+EXPORTS = ("ssmq_state_update", "ssmq_state_update_ex", "ssmq_conv1d_update", "ssmq_requantize",
+           "ssmq_dither_fill", "ssmq_status_string", "ssmq_last_error")
 
 _lib = None
 
@@ -58,6 +62,12 @@ def library() -> ctypes.CDLL:
     L.ssmq_state_update.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(QParams), _vp, _vp, _vp,
                                     _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.ssmq_state_update.restype = _i32
+    L.ssmq_state_update_ex.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(QParams),
+                                       ctypes.POINTER(StepOpts), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                       _vp, _vp, _vp]
+    L.ssmq_state_update_ex.restype = _i32
+    L.ssmq_conv1d_update.argtypes = [_i64, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp]
+    L.ssmq_conv1d_update.restype = _i32
     L.ssmq_requantize.argtypes = [ctypes.POINTER(QParams), _i64, _i64, _vp, _vp, _vp, _vp]
     L.ssmq_requantize.restype = _i32
     L.ssmq_dither_fill.argtypes = [_i32, _u32, _u32, _u32, _u64, _i64, _i32, _vp, _vp]
@@ -107,7 +117,7 @@ def qparams(rule: str, fmt: str, *, dither_block=16, scale_group=0, seed=0, laye
 
 def state_update(state, scale, x, dt, A, B, C, D, y, *, rule: str, fmt: str, dither_block=16,
                  scale_group=0, seed=0, layer=0, step=0, entry_base=0, fp32_state=False,
-                 stream=None) -> None:
+                 dt_bias=None, dt_softplus=False, z=None, stream=None) -> None:
     """ssmq_state_update on [batch, nheads, headdim, dstate] state codes, in place
     (INT4: [batch, nheads, headdim, dstate / 2] bytes). fp32_state: a checkpoint
     write on an fp32 state [batch, nheads, headdim, dstate] (SSMQ_FLAG_FP32_STATE)."""
@@ -123,9 +133,25 @@ def state_update(state, scale, x, dt, A, B, C, D, y, *, rule: str, fmt: str, dit
     q = qparams(rule, fmt, dither_block=dither_block, scale_group=scale_group, seed=seed,
                 layer=layer, step=step, entry_base=entry_base,
                 flags=FLAG_FP32_STATE if fp32_state else 0)
-    _check(library().ssmq_state_update(ctypes.byref(dims), ctypes.byref(q), _ptr(state),
-                                       _ptr(scale), _ptr(x), _ptr(dt), _ptr(A), _ptr(B), _ptr(C),
-                                       _ptr(D), _ptr(y), _stream(stream, state)))
+    if dt_bias is None and not dt_softplus and z is None:
+        _check(library().ssmq_state_update(ctypes.byref(dims), ctypes.byref(q), _ptr(state),
+                                           _ptr(scale), _ptr(x), _ptr(dt), _ptr(A), _ptr(B),
+                                           _ptr(C), _ptr(D), _ptr(y), _stream(stream, state)))
+    else:
+        opts = StepOpts(_ptr(dt_bias), 1 if dt_softplus else 0, 0, _ptr(z))
+        _check(library().ssmq_state_update_ex(ctypes.byref(dims), ctypes.byref(q),
+                                              ctypes.byref(opts), _ptr(state), _ptr(scale),
+                                              _ptr(x), _ptr(dt), _ptr(A), _ptr(B), _ptr(C),
+                                              _ptr(D), _ptr(y), _stream(stream, state)))
+
+
+def conv1d_update(conv_state, x, weight, bias, out, *, act=True, stream=None) -> None:
+    """ssmq_conv1d_update: conv_state [batch, channels, width] shifted in place,
+    out [batch, channels] written."""
+    batch, channels, width = conv_state.shape
+    _check(library().ssmq_conv1d_update(batch, channels, width, _ptr(conv_state), _ptr(x),
+                                        _ptr(weight), _ptr(bias), 1 if act else 0, _ptr(out),
+                                        _stream(stream, conv_state)))
 
 
 def requantize(h, codes, scale, *, rule: str, fmt: str, head_size=0, dither_block=16,

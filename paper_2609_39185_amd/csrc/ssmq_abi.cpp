@@ -123,7 +123,18 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
                               float* state_scale, const float* x, const float* dt,
                               const float* A, const float* B, const float* C, const float* D,
                               float* y, void* stream) {
+  return ssmq_state_update_ex(dims, q, nullptr, state, state_scale, x, dt, A, B, C, D, y, stream);
+}
+
+ssmq_status ssmq_state_update_ex(const ssmq_dims* dims, const ssmq_qparams* q,
+                                 const ssmq_step_opts* opts, void* state, float* state_scale,
+                                 const float* x, const float* dt, const float* A, const float* B,
+                                 const float* C, const float* D, float* y, void* stream) {
   if (!dims) return fail(SSMQ_EINVAL, "dims is NULL");
+  if (opts && (opts->reserved != 0 || (opts->dt_softplus != 0 && opts->dt_softplus != 1)))
+    return fail(SSMQ_EINVAL, "opts: dt_softplus must be 0 or 1 and reserved 0");
+  if (opts && ((opts->dt_bias && !aligned(opts->dt_bias, 4)) || (opts->z && !aligned(opts->z, 4))))
+    return fail(SSMQ_EALIGN, "dt_bias and z must be 4-byte aligned");
   ssmq_status st = check_qparams(q);
   if (st != SSMQ_OK) return st;
   const ssmq_dims& d = *dims;
@@ -167,6 +178,11 @@ ssmq_status ssmq_state_update(const ssmq_dims* dims, const ssmq_qparams* q, void
   ssmq::UpdateArgs a{};
   a.state = state; a.scale = state_scale; a.x = x; a.dt = dt; a.A = A; a.B = B; a.C = C;
   a.D = D; a.y = y;
+  if (opts) {
+    a.dt_bias = opts->dt_bias;
+    a.dt_softplus = opts->dt_softplus;
+    a.z = opts->z;
+  }
   a.batch = d.batch; a.nheads = d.nheads; a.headdim = d.headdim; a.dstate = d.dstate;
   a.ngroups = d.ngroups; a.heads_per_group = d.nheads / d.ngroups;
   a.lanes_per_row = d.dstate / V; a.lr_shift = log2i(a.lanes_per_row);
@@ -266,6 +282,31 @@ ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t he
   if (!scaled && (n_entries + 16 * 256 - 1) / (16 * 256) > 0x7FFFFFFFLL)
     return fail(SSMQ_EUNSUPPORTED, "too many entries for one launch");
   hipError_t e = ssmq::launch_requant(a, q->format, q->rule, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+ssmq_status ssmq_conv1d_update(int64_t batch, int32_t channels, int32_t width, float* conv_state,
+                               const float* x, const float* weight, const float* bias,
+                               int32_t act, float* out, void* stream) {
+  if (batch < 0) return fail(SSMQ_EINVAL, "batch < 0");
+  if (channels < 1 || width < 1 || width > 64)
+    return fail(SSMQ_EINVAL, "channels must be >= 1 and width in [1, 64]");
+  if (act != 0 && act != 1) return fail(SSMQ_EINVAL, "act must be 0 or 1");
+  if (batch == 0) return ok();
+  if (!conv_state || !x || !weight || !out)
+    return fail(SSMQ_EINVAL, "conv_state, x, weight and out must not be NULL");
+  if (!aligned(conv_state, 4) || !aligned(x, 4) || !aligned(weight, 4) || !aligned(out, 4) ||
+      (bias && !aligned(bias, 4)))
+    return fail(SSMQ_EALIGN, "conv1d arrays must be 4-byte aligned");
+  int64_t n = 0;
+  if (!mul_ok(batch, channels, &n) || n > 0xFFFFFFFFLL)
+    return fail(SSMQ_EUNSUPPORTED, "batch * channels must be below 2^32");
+  ssmq::ConvArgs a{};
+  a.state = conv_state; a.x = x; a.weight = weight; a.bias = bias; a.out = out;
+  a.n = n; a.channels = channels; a.width = width; a.act = act;
+  a.div_channels = ssmq::make_fastdiv(static_cast<uint32_t>(channels));
+  hipError_t e = ssmq::launch_conv1d(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
   return ok();
 }

@@ -36,6 +36,16 @@ __device__ inline float decay(float dtv, float a) {
   return static_cast<float>(exp(static_cast<double>(dtv * a)));  // correctly rounded fl32(exp)
 }
 
+// The step size the update uses: dt, plus dt_bias[head] when given, through
+// softplus(v) = log(1 + e^v) (double, one rounding; v itself above 20) when asked.
+__device__ inline float step_size(const UpdateArgs& a, float dtv, int head) {
+  if (a.dt_bias) dtv = dtv + a.dt_bias[head];
+  if (a.dt_softplus && !(dtv > 20.0f)) dtv = static_cast<float>(log1p(exp(static_cast<double>(dtv))));
+  return dtv;
+}
+
+__device__ inline float silu(float v) { return v / (1.0f + expf(-v)); }
+
 // ---------------------------------------------------------------------------
 // Mamba-2 head slabs: NT threads x CPT chunks = a run of whole rows of one head.
 // ---------------------------------------------------------------------------
@@ -71,14 +81,14 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
     raw[j] = load_stream<chunk_t<F>>(hstate + chunk_bytes_at<F>(l0 + j * pass));
     xv[j] = hx[r0 + j * rows_per_pass];
   }
-  const float dtv = a.dt[tile];
+  const float dt_in = a.dt[tile];
   const float Dv = a.D ? a.D[hh] : 0.0f;
 
   // Per-head values are staged once per workgroup in LDS while the state loads
   // are in flight: B and C of the head's group (one float4 per thread), and
   // exp(dt A), evaluated by the first wave in double with one final rounding.
   __shared__ float4 sBC[kMaxDstate / 2];
-  __shared__ float sh[2];
+  __shared__ float sh[3];
   const int nq = a.dstate >> 2;  // float4 per vector
   const float* Bg = a.B + (b * a.ngroups + g) * a.dstate;
   const float* Cg = a.C + (b * a.ngroups + g) * a.dstate;
@@ -86,11 +96,13 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
     sBC[i] = (i < nq) ? reinterpret_cast<const float4*>(Bg)[i]
                       : reinterpret_cast<const float4*>(Cg)[i - nq];
   if (t < 64) {
-    const float d = decay(dtv, a.A[hh]);
-    if (t == 0) sh[0] = d;
+    const float dte = step_size(a, dt_in, hh);
+    const float d = decay(dte, a.A[hh]);
+    if (t == 0) { sh[0] = d; sh[2] = dte; }
   }
   __syncthreads();
   const float dA = sh[0];
+  const float dtv = sh[2];
 
   float h[CPT][V];
   bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
@@ -123,7 +135,11 @@ __global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
     }
     bad[j] = !__builtin_isfinite(ys);
     ys = lane_sum(ys, a.lanes_per_row);
-    if (cc == 0) hy[r0 + j * rows_per_pass] = ys + Dv * xv[j];
+    if (cc == 0) {
+      float yv = ys + Dv * xv[j];
+      if (a.z) yv = yv * silu(a.z[tile * a.headdim + r0 + j * rows_per_pass]);
+      hy[r0 + j * rows_per_pass] = yv;
+    }
   }
 
   float r[CPT];  // scaled formats: 1 / s of each chunk's group
@@ -222,7 +238,7 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
     decode_chunk<F>(load_stream<chunk_t<F>>(state + chunk_bytes_at<F>(e)), hp);
   }
   const float xv = a.x[row];
-  const float dtv = a.dt[bh];
+  const float dtv = step_size(a, a.dt[bh], hh);
   const float Dv = a.D ? a.D[hh] : 0.0f;
   float Bv[V], Cv[V], dA[V];
   load_floats<V>(a.B + (static_cast<int64_t>(b) * a.ngroups + g) * a.dstate + n0, Bv);
@@ -252,7 +268,7 @@ __global__ __launch_bounds__(256) void k_update_rows(UpdateArgs a) {
   }
   const bool bad = !__builtin_isfinite(ys);
   ys = lane_sum(ys, a.lanes_per_row);
-  if (live && cc == 0) a.y[row] = ys + Dv * xv;
+  if (live && cc == 0) a.y[row] = a.z ? (ys + Dv * xv) * silu(a.z[row]) : ys + Dv * xv;
   float rs = 1.0f, s = 1.0f;
   if constexpr (Traits<F>::scaled) {
     float m = 0.0f;
@@ -373,6 +389,26 @@ __global__ __launch_bounds__(256) void k_dither_fill(DitherArgs a) {
     const uint64_t ge = a.entry_base + static_cast<uint64_t>(e + k);
     a.out[e + k] = (R == kRTN) ? (1u << 23) : (entry_thr<R>(ge, a.thr) >> 8);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Causal depthwise conv1d decode update: thread i = b * channels + c shifts its
+// channel's window by one, appends x[i] and writes
+// out[i] = (silu)(bias[c] + sum_k window[k] * weight[c][k]).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_conv1d_update(ConvArgs a) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= a.n) return;
+  const uint32_t c = static_cast<uint32_t>(i) - a.div_channels.div(static_cast<uint32_t>(i)) * a.channels;
+  float* const st = a.state + i * a.width;
+  const float* const w = a.weight + static_cast<int64_t>(c) * a.width;
+  float acc = a.bias ? a.bias[c] : 0.0f;
+  for (int k = 0; k < a.width; ++k) {
+    const float v = (k + 1 < a.width) ? st[k + 1] : a.x[i];
+    st[k] = v;
+    acc = fmaf(v, w[k], acc);
+  }
+  a.out[i] = a.act ? silu(acc) : acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -499,6 +535,12 @@ hipError_t launch_dither(const DitherArgs& a, int rule, hipStream_t s) {
     case kPHILOX: hipLaunchKernelGGL((k_dither_fill<kPHILOX>), dim3(grid), dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((k_dither_fill<kWEYL>), dim3(grid), dim3(256), 0, s, a); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_conv1d(const ConvArgs& a, hipStream_t s) {
+  const unsigned grid = static_cast<unsigned>((a.n + 255) / 256);
+  hipLaunchKernelGGL(k_conv1d_update, dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

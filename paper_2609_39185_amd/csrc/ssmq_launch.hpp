@@ -58,6 +58,9 @@ struct UpdateArgs {
   const float* C;
   const float* D;
   float* y;
+  const float* dt_bias;     // [nheads] added to dt, or null
+  const float* z;           // [batch][nheads][headdim] gate y <- y * silu(z), or null
+  int32_t dt_softplus;      // dt <- softplus(dt + dt_bias)
   int64_t batch;
   int32_t nheads, headdim, dstate, ngroups;
   int32_t heads_per_group;
@@ -90,6 +93,17 @@ struct RequantArgs {
   uint32_t toff[16];
 };
 
+struct ConvArgs {
+  float* state;             // [n][width]
+  const float* x;           // [n]
+  const float* weight;      // [channels][width]
+  const float* bias;        // [channels] or null
+  float* out;               // [n]
+  int64_t n;                // batch * channels
+  int32_t channels, width, act;
+  FastDiv div_channels;
+};
+
 struct DitherArgs {
   uint32_t* out;
   int64_t n;
@@ -101,5 +115,6 @@ hipError_t launch_update(const UpdateArgs& a, int format, int rule, int cfg, boo
                          hipStream_t s);
 hipError_t launch_requant(const RequantArgs& a, int format, int rule, hipStream_t s);
 hipError_t launch_dither(const DitherArgs& a, int rule, hipStream_t s);
+hipError_t launch_conv1d(const ConvArgs& a, hipStream_t s);
 
 }  // namespace ssmq

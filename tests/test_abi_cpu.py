@@ -35,6 +35,24 @@ def test_exports_every_declared_function(lib):
         assert hasattr(L, name), name
 
 
+def test_conv1d_and_options_validation(lib):
+    L = lib.library()
+    c = L.ssmq_conv1d_update
+    assert c(1, 0, 4, FAKE, FAKE, FAKE, None, 1, FAKE, None) == EINVAL       # no channels
+    assert c(1, 8, 65, FAKE, FAKE, FAKE, None, 1, FAKE, None) == EINVAL      # width
+    assert c(1, 8, 4, FAKE, FAKE, FAKE, None, 2, FAKE, None) == EINVAL       # act
+    assert c(1, 8, 4, None, FAKE, FAKE, None, 1, FAKE, None) == EINVAL       # null state
+    assert c(1, 8, 4, FAKE + 2, FAKE, FAKE, None, 1, FAKE, None) == EALIGN
+    assert c(0, 8, 4, None, None, None, None, 1, None, None) == 0            # empty batch
+    dims = lib.Dims(1, 4, 64, 128, 2, 0)
+    q = lib.qparams("weyl", "bf16")
+    for opts, want in ((lib.StepOpts(None, 2, 0, None), EINVAL), (lib.StepOpts(None, 1, 1, None), EINVAL),
+                       (lib.StepOpts(FAKE + 2, 1, 0, None), EALIGN)):
+        assert L.ssmq_state_update_ex(ctypes.byref(dims), ctypes.byref(q), ctypes.byref(opts),
+                                      FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                      None) == want
+
+
 def test_status_strings(lib):
     L = lib.library()
     assert L.ssmq_status_string(0) == b"ok"

@@ -1,0 +1,94 @@
+"""GPU parity of the decode-step operations around the update (Appendix B
+"Runners"): dt' = softplus(dt + dt_bias) and y' = y * silu(z) fused into the
+update (ssmq_state_update_ex), and the causal depthwise conv1d decode update
+(ssmq_conv1d_update), against the oracle through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_39185_amd import workloads as wl
+
+from ._parity import DEV, assert_codes, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ssmq():
+    import paper_2609_39185_amd as m
+    m.library()
+    return m
+
+
+CASES = [("bf16", "weyl", "mamba2", (2, 4, 64, 128, 2), {"dither_block": 128}),
+         ("e4m3", "sr", "mamba2", (2, 4, 64, 128, 2), {"dither_block": 128}),
+         ("int8", "weyl", "mamba2", (2, 4, 64, 128, 2), {"scale_group": 128, "dither_block": 128}),
+         ("fp16", "weyl", "mamba1", (3, 200, 1, 16, 1), {}),
+         ("int4", "philox", "mamba1", (2, 96, 1, 16, 1), {"scale_group": 16})]
+
+
+@pytest.mark.parametrize("fmt,rule,family,shape,q", CASES)
+@pytest.mark.parametrize("softplus,bias,gate", [(True, True, True), (True, False, False),
+                                                (False, True, False), (False, False, True)])
+def test_step_with_dt_bias_softplus_and_gate(ssmq, fmt, rule, family, shape, q, softplus, bias,
+                                             gate):
+    b, h, p, n, g = shape
+    say(f"case decode ops {fmt} {rule} {family} {shape} softplus={softplus} bias={bias} gate={gate}")
+    A, D = wl.layer_params(family, h, n, 120)
+    x, dt, B, C = wl.step_inputs(b, h, p, n, g, 121)
+    rng = np.random.default_rng(122)
+    dt_raw = torch.from_numpy((rng.standard_normal((b, h)) * 2 - 3).astype(np.float32))
+    dt_bias = torch.from_numpy(rng.uniform(-4, 1, h).astype(np.float32)) if bias else None
+    z = torch.from_numpy(rng.standard_normal((b, h, p)).astype(np.float32)) if gate else None
+    if not softplus:
+        dt_raw = dt_raw.abs() * 0.05
+    codes, scale = wl.initial_state(fmt, b, h, p, n, 123, group=q.get("scale_group", 0))
+    st = codes.to(DEV)
+    sc = None if scale is None else scale.to(DEV)
+    y = torch.empty((b, h, p), device=DEV)
+    ssmq.state_update(st, sc, x.to(DEV), dt_raw.to(DEV), A.to(DEV), B.to(DEV), C.to(DEV),
+                      D.to(DEV), y, rule=rule, fmt=fmt, step=6, layer=2,
+                      dt_bias=None if dt_bias is None else dt_bias.to(DEV), dt_softplus=softplus,
+                      z=None if z is None else z.to(DEV), **q)
+    torch.cuda.synchronize()
+    r_codes, r_scale, r_y, r_h = oracle.state_update(
+        fmt, rule, wl.to_numpy_codes(fmt, codes), None if scale is None else scale.numpy(),
+        x.numpy(), dt_raw.numpy(), A.numpy(), B.numpy(), C.numpy(), D.numpy(), step=6, layer=2,
+        block=q.get("dither_block", 16), group=q.get("scale_group", 0),
+        dt_bias=None if dt_bias is None else dt_bias.numpy(), dt_softplus=softplus,
+        z=None if z is None else z.numpy())
+    assert_codes(fmt, wl.to_numpy_codes(fmt, st.cpu()), r_codes, "decode ops")
+    if sc is not None:
+        np.testing.assert_array_equal(sc.cpu().numpy(), r_scale)
+    Ch = np.repeat(C.numpy().astype(np.float64), h // g, axis=1)[:, :, None, :]
+    mag = np.abs(Ch * r_h.astype(np.float64)).sum(-1) + np.abs(D.numpy()[None, :, None] * x.numpy())
+    if z is not None:
+        mag = mag * np.abs(torch.nn.functional.silu(z.double()).numpy())
+    err = np.abs(y.cpu().numpy().astype(np.float64) - r_y)
+    assert np.all(err <= 1e-5 * (mag + np.abs(r_y)) + 1e-30), err.max()
+
+
+@pytest.mark.parametrize("batch,channels,width", [(1, 7, 4), (3, 1536, 4), (2, 8192 + 2 * 8 * 128, 4),
+                                                  (5, 33, 1), (2, 100, 7), (0, 16, 4)])
+@pytest.mark.parametrize("act", [True, False])
+def test_conv1d_update(ssmq, batch, channels, width, act):
+    say(f"case conv1d b{batch} c{channels} w{width} act={act}")
+    rng = np.random.default_rng(channels + width)
+    state = rng.standard_normal((batch, channels, width)).astype(np.float32)
+    x = rng.standard_normal((batch, channels)).astype(np.float32)
+    w = rng.standard_normal((channels, width)).astype(np.float32)
+    bias = rng.standard_normal(channels).astype(np.float32) if width != 7 else None
+    st = torch.from_numpy(state).to(DEV)
+    out = torch.full((batch, channels), float("nan"), device=DEV)
+    ssmq.conv1d_update(st, torch.from_numpy(x).to(DEV), torch.from_numpy(w).to(DEV),
+                       None if bias is None else torch.from_numpy(bias).to(DEV), out, act=act)
+    torch.cuda.synchronize()
+    r_state, r_out = oracle.conv1d_update(state, x, w, bias, act=act)
+    assert np.array_equal(st.cpu().numpy(), r_state)
+    window = r_state.astype(np.float64)
+    mag = np.abs(window * w[None].astype(np.float64)).sum(-1)
+    if bias is not None:
+        mag = mag + np.abs(bias.astype(np.float64))[None]
+    err = np.abs(out.cpu().numpy().astype(np.float64) - r_out)
+    assert np.all(err <= 1e-5 * (mag + np.abs(r_out)) + 1e-30), err.max() if err.size else 0
