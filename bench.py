@@ -8,7 +8,10 @@ each layer keeps one input set across steps while the step counter t advances.
 
 Prints one JSON line. `value` is the state read+write bandwidth (GB/s) of the
 headline variant (bf16 state, Weyl dither); the other formats and rules are
-reported under "variants".
+reported under "variants". Each variant's timed region is exactly --steps steps
+between two events on the launch stream; since that stream carries only the
+update launches, the region's time over their number is the average launch
+duration behind roofline.achieved.
 """
 from __future__ import annotations
 
@@ -141,26 +144,34 @@ def main() -> int:
 
     results = {}
     t_global = 1
+    launches = args.steps * L
     for fmt, rule in variants:
         for _ in range(args.warmup):
             one_step(fmt, rule, t_global)
             t_global += 1
         torch.cuda.synchronize()
-        ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(L)]
-              for _ in range(args.steps)]
+        # Timed region: exactly --steps steps between two events on the launch stream.
+        # The stream holds only the update launches, so the region's time divided by
+        # their number is the average launch duration (gaps included).
         start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         start.record(stream)
         for k in range(args.steps):
-            one_step(fmt, rule, t_global, ev[k])
+            one_step(fmt, rule, t_global)
             t_global += 1
         stop.record(stream)
         torch.cuda.synchronize()
         total_ms = start.elapsed_time(stop)
-        launch_ms = [e[0].elapsed_time(e[1]) for step_ev in ev for e in step_ev]
         ms_step = total_ms / args.steps
+        avg_launch_ms = total_ms / launches
+        # Diagnostic only: one more step with events around every launch (each pair
+        # adds a few microseconds, so these durations run long).
+        ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(L)]]
+        one_step(fmt, rule, t_global, ev[0])
+        t_global += 1
+        torch.cuda.synchronize()
+        per_launch = [e[0].elapsed_time(e[1]) for e in ev[0]]
         sbytes = state_bytes_per_launch(w, fmt)
-        avg_launch_ms = sum(launch_ms) / len(launch_ms)
         results[f"{fmt}:{rule}"] = {
             "ms_per_step": ms_step,
             "steps_per_s": 1000.0 / ms_step,
@@ -169,6 +180,9 @@ def main() -> int:
             "kernel_avg_us": avg_launch_ms * 1e3,
             "kernel_state_GBps": sbytes / (avg_launch_ms * 1e6),
             "state_bytes_per_launch": sbytes,
+            "event_bracketed_launch_us": {"avg": 1e3 * sum(per_launch) / len(per_launch),
+                                          "min": 1e3 * min(per_launch),
+                                          "max": 1e3 * max(per_launch)},
         }
 
     # ---- streaming ceiling: a plain elementwise kernel of known size ----------------

@@ -49,8 +49,13 @@ __device__ inline float silu(float v) { return v / (1.0f + expf(-v)); }
 // ---------------------------------------------------------------------------
 // Mamba-2 head slabs: NT threads x CPT chunks = a run of whole rows of one head.
 // ---------------------------------------------------------------------------
+// The whole-head configurations of the scaled formats (four chunks per thread,
+// up to 128 threads) hold 64 state values per thread and sit at the 128-register
+// line; they are held to it (four waves per SIMD), at the price of a few bytes
+// of spilled addresses, instead of dropping to three waves.
 template <int F, int R, int NT, int CPT>
-__global__ __launch_bounds__(NT) void k_update_slab(UpdateArgs a) {
+__global__ __launch_bounds__(NT, (Traits<F>::scaled && CPT == 4 && NT <= 128) ? 4 : 1)
+void k_update_slab(UpdateArgs a) {
   constexpr int V = Traits<F>::V;
   constexpr int NW = NT / 64;
   const int t = threadIdx.x;
