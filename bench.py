@@ -310,7 +310,7 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
     scale). memory: "short" (the throughput bench's decay rates) or "trained" (a
     trained model's spread, workloads.layer_params_trained_memory). cc > 0 adds,
     for RTN, SR (seed 0) and Weyl, a periodically checkpointed run: an fp32 state
-    rounded onto the format's grid at every cc-th write only (Section 5 "Periodic
+    rounded onto the format's grid at every cc-th write only (Section 6.5 "Periodic
     checkpointing").
 
     Inputs: A, D per layer; x, dt, B, C for all layers of step t from one generator

@@ -78,7 +78,7 @@ typedef struct {
 
 /*
  * SSMQ_FLAG_FP32_STATE (ssmq_state_update only): a checkpoint write on an fp32
- * state, for periodic checkpointing (Section 5 "Periodic checkpointing";
+ * state, for periodic checkpointing (Section 6.5 "Periodic checkpointing";
  * Appendix B "Decode regime", CC = 8: fp32 intermediate states, rounding every
  * k-th write). `state` holds fp32 values, read as they are; each new value is
  * rounded onto the grid of q->format under q->rule (E4M3/INT8/INT4 with their
@@ -102,7 +102,7 @@ typedef struct {
                               The paper's blocks: 16 (Mamba), 128 (hybrids)               */
     uint32_t seed;         /* sigma (Appendix B "Dithers"; SR key)                          */
     uint32_t layer;        /* l (Appendix B "Dithers"; SR key)                              */
-    uint32_t step;         /* t, the integer phase counter (Section 5.4, "Computing the
+    uint32_t step;         /* t, the integer phase counter (Section 6.4, "Computing the
                               phase in float32": an integer phase keeps every stream)      */
     uint32_t flags;        /* 0, or SSMQ_FLAG_FP32_STATE                                    */
     uint64_t entry_base;   /* global flat index of entry 0 of this tensor, a multiple of
@@ -219,7 +219,7 @@ ssmq_status ssmq_requantize(const ssmq_qparams* q, int64_t n_entries, int64_t he
  *   SSMQ_WEYL: top 24 bits of (A(r+1) + B(c+1) + L layer + S seed + t Phi) mod 2^32,
  *              r = i / dither_block, c = i % dither_block; A, B, L, S are 2^32 times
  *              0.7548776662, 0.5698402910, 0.1234567, 0.3141592 rounded to nearest and
- *              Phi = 2654435769 (Appendix B "Dithers"; Section 5.4).
+ *              Phi = 2654435769 (Appendix B "Dithers"; Section 6.4).
  *   SSMQ_SR:   top 24 bits of fmix32(i * 0x9E3779B1 + K) with the per-step key
  *              K = fmix32(fmix32(fmix32(seed) ^ layer * 0xC2B2AE3D) ^ t * 0x85EBCA77)
  *              (Appendix B "Decode regime", hash SR; fmix32 = MurmurHash3 finalizer).

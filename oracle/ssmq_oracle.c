@@ -267,7 +267,7 @@ static int32_t int_value(int f, uint32_t code) {
  *   acc = A (r+1) + B (c+1) + L l + S sigma + t Phi   (mod 2^32),
  * whose top 24 bits are the threshold. A, B, L, S are the decimal constants of
  * the float form times 2^32, rounded to the nearest integer; Phi is the 32-bit
- * golden increment (Section 5.4, Observation on aliasing).
+ * golden increment (Section 6.4 "Three silent pitfalls", Observation "Space-time aliasing").
  * r = i / block, c = i % block for the flat entry index i.
  */
 static uint32_t W_A, W_B, W_L, W_S;
@@ -663,7 +663,7 @@ int orc_state_update_ex(int f, int rule, uint32_t seed, uint32_t layer, uint32_t
 }
 
 /*
- * Checkpoint write with an fp32 state (Section 5 "Periodic checkpointing";
+ * Checkpoint write with an fp32 state (Section 6.5 "Periodic checkpointing";
  * Appendix B "Decode regime", CC = 8: fp32 intermediate states, rounding at
  * every k-th write). The state holds fp32 values. One step of eq. (rec) is
  * taken in fp32 exactly as for the unrounded format (h_prev is the stored

@@ -50,7 +50,7 @@ enum Rule : int { kRTN = 0, kSR = 1, kWEYL = 2, kPHILOX = 3 };
 
 // Weyl accumulator (Appendix B "Dithers", hardware form): 2^32 times
 // 0.7548776662, 0.5698402910, 0.1234567, 0.3141592, rounded to nearest, and the
-// 32-bit golden increment (Section 5.4).
+// 32-bit golden increment (Section 6.4 "Three silent pitfalls").
 constexpr uint32_t kWeylA = 0xC13FA9A9u;
 constexpr uint32_t kWeylB = 0x91E10DA6u;
 constexpr uint32_t kWeylL = 0x1F9ADBB9u;

@@ -1,5 +1,5 @@
 """GPU parity of the checkpoint write on an fp32 state (SSMQ_FLAG_FP32_STATE;
-Section 5 "Periodic checkpointing", Appendix B "Decode regime" CC = 8) against the
+Section 6.5 "Periodic checkpointing", Appendix B "Decode regime" CC = 8) against the
 oracle, through the C ABI: each fp32 value rounded onto a format's grid."""
 import numpy as np
 import pytest

@@ -1,4 +1,4 @@
-"""Pins of the oracle's checkpoint write on an fp32 state (Section 5 "Periodic
+"""Pins of the oracle's checkpoint write on an fp32 state (Section 6.5 "Periodic
 checkpointing"; Appendix B "Decode regime", CC = 8): one fp32 step of eq. (rec),
 then every value rounded onto a format's grid and kept as fp32.
 

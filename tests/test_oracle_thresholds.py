@@ -1,11 +1,15 @@
 """Pins of the oracle's threshold generators (CPU only).
 
-Expected values come from the paper: the Weyl time sequence 0.618, 0.236,
-0.854 (Section 1), the 32-bit golden increment 2654435769 and Knuth's constant
-2654435761 (Section 5.4), the R2 offset constants and the separation d = 0.0015
-(Appendix B "Offset near-aliasing" and "Dithers"), Observation 2's stream counts
-for a float32 phase, the LD_256 column of Table "Dither sequences" and the
-hash-SR unit-test moments (Appendix B "Decode regime").
+Expected values the paper prints are read from tests/golden/ (each file names
+its passage): the Weyl time sequence (Section 1), Observation "Phase precision"'s
+stream counts for a float32 phase, the separation d of the R2 and Knuth offsets
+(Appendix B "Offset near-aliasing"), the LD_256 column of Table "Dither
+sequences" and the hash-SR unit-test moments (Appendix B "Decode regime"). The
+rest rests on mathematics: the decimal constants times 2^32 (Appendix B
+"Dithers"), the golden increment and Knuth's constant 2654435761 (Section 6.4
+"Three silent pitfalls"), the closed form of the fractional parts of t alpha,
+the correlation 1 - 6 d (1 - d) of two rotated streams, and the Philox4x32-10
+known answers of its authors.
 """
 from decimal import Decimal, getcontext
 
@@ -13,6 +17,8 @@ import numpy as np
 import pytest
 
 from oracle import discrepancy as dsc
+
+from ._golden import records, table
 
 TWO24 = 1 << 24
 TWO32 = 1 << 32
@@ -36,7 +42,13 @@ def test_weyl_time_sequence(orc, entry):
     """Per entry the thresholds advance by alpha = phi - 1: 0.618, 0.236, 0.854 ..."""
     U = np.array([orc.thresholds("weyl", 3, 7, t, entry, 1, 16)[0] for t in range(4)], np.int64)
     steps = ((U[1:] - U[0]) % TWO24) / TWO24
-    assert np.allclose(steps, [0.618034, 0.236068, 0.854102], atol=2e-6)
+    printed = records("weyl_time_sequence.txt")
+    assert [int(r[0]) for r in printed] == [1, 2, 3]
+    assert np.allclose(steps, [float(r[1]) for r in printed], atol=5e-4)   # three decimals
+    getcontext().prec = 40
+    alpha = (Decimal(5).sqrt() - 1) / 2
+    exact = [float((t * alpha) % 1) for t in (1, 2, 3)]
+    assert np.allclose(steps, exact, atol=2 ** -24 * 2)  # 24-bit thresholds of a 32-bit phase
 
 
 def test_weyl_float_form_agrees_for_small_indices(orc):
@@ -57,12 +69,30 @@ def test_weyl_float_form_agrees_for_small_indices(orc):
 
 
 def test_r2_offsets_separation(orc):
+    printed = table("offset_separation.txt")
     k = orc.weyl_constants()
     beta, gamma, alpha = k["A"] / TWO32, k["B"] / TWO32, k["PHI"] / TWO32
     d = dsc.separation(beta, gamma, alpha)
-    assert 0.0014 <= d <= 0.0016                 # the paper: d = 0.0015
+    assert abs(d - printed["r2"][0]) <= 0.5e-4   # printed to four decimals
     knuth = 2654435761 / TWO32
-    assert dsc.separation(knuth, knuth, alpha) < 1e-8   # Knuth offsets alias exactly
+    assert dsc.separation(knuth, knuth, alpha) <= printed["knuth"][0] + 8 / TWO32  # exact aliasing
+
+
+def test_rotated_streams_correlate_as_one_minus_6d(orc):
+    """Two entries whose offsets differ by dr beta + dc gamma, compared l steps apart,
+    are rotations by delta = {dr beta + dc gamma + l alpha}: over time their
+    thresholds correlate as 1 - 6 delta (1 - delta)."""
+    k = orc.weyl_constants()
+    beta, gamma, alpha = k["A"] / TWO32, k["B"] / TWO32, k["PHI"] / TWO32
+    block, r0, c0, T = 16, 5, 6, 6000
+    U = np.stack([orc.thresholds("weyl", 0, 0, t, 0, block * 10, block) for t in range(T + 20)])
+    U = U.astype(np.float64) / TWO24
+    for dr, dc, lag in ((1, 0, 0), (0, 1, 0), (1, 2, 3), (-2, 1, 5), (2, -2, 16), (1, 1, 0)):
+        i1, i2 = r0 * block + c0, (r0 + dr) * block + (c0 + dc)
+        a, b = U[:T, i1], U[lag:T + lag, i2]
+        delta = (dr * beta + dc * gamma + lag * alpha) % 1.0
+        corr = np.corrcoef(a, b)[0, 1]
+        assert abs(corr - (1 - 6 * delta * (1 - delta))) < 4e-3, (dr, dc, lag, corr, delta)
 
 
 def test_knuth_offsets_alias_with_time(orc):
@@ -82,7 +112,9 @@ def test_float32_phase_collapses_streams(orc):
     """Observation 2: a float32 phase leaves at most 2^(p-1-k) streams; the integer one keeps all."""
     alpha32 = np.float32((5 ** 0.5 - 1) / 2)
     offsets = (np.arange(1 << 16, dtype=np.float64) / (1 << 16)).astype(np.float32)
-    for t, expect in ((2047, 8192), (8191, 2048), (32767, 512)):
+    printed = [(int(t), int(n)) for t, n in records("float32_phase_streams.txt")]
+    assert len(printed) == 3
+    for t, expect in printed:
         phase = np.float32(np.float32(t) * alpha32)
         s = (offsets + phase).astype(np.float32)
         frac = (s - np.floor(s)).astype(np.float32)
@@ -106,34 +138,42 @@ def _windows_weyl_oracle(orc, rng, count, W=256):
 def test_ld256_table(orc):
     """LD_256 of Table "Dither sequences" (64 random phases; paper values +-12%)."""
     rng = np.random.default_rng(2026)
+    printed = {k: v[0] for k, v in table("dither_sequences_ld256.txt").items()}
 
-    def ld_float(alpha):
+    def ld_float(alpha, windows=64):
         return dsc.local_discrepancy([dsc.weyl_float(alpha, rng.random(), int(rng.integers(0, 1 << 20)),
-                                                     256) for _ in range(64)])
+                                                     256) for _ in range(windows)])
 
-    phi1 = (5 ** 0.5 - 1) / 2
-    table = {
-        2 ** 0.5 - 1: 0.0069,
-        1 / (2 + (1 + 5 ** 0.5) / 2): 0.0075,
-        phi1: 0.0078,
-        np.e - 2: 0.0097,
-        0.25 + 2 ** -12: 0.1379,
-        1 / 3 + 2 ** -12: 0.2063,
-        0.5 + 2 ** -12: 0.3347,
+    phi = (1 + 5 ** 0.5) / 2
+    increments = {
+        "weyl:sqrt2-1": 2 ** 0.5 - 1,
+        "weyl:1/(2+phi)": 1 / (2 + phi),
+        "weyl:phi-1": phi - 1,
+        "weyl:e-2": np.e - 2,
+        "weyl:1/4+2^-12": 0.25 + 2 ** -12,
+        "weyl:1/3+2^-12": 1 / 3 + 2 ** -12,
+        "weyl:1/2+2^-12": 0.5 + 2 ** -12,
     }
-    for alpha, paper in table.items():
-        assert abs(ld_float(alpha) / paper - 1) < 0.12, alpha
+    assert set(increments) | {"sr", "weyl:per-entry-uniform[0.2,0.8]"} == set(printed)
+    for name, alpha in increments.items():
+        assert abs(ld_float(alpha) / printed[name] - 1) < 0.12, name
+    # one increment per entry, drawn from U[0.2, 0.8]: the mean is dominated by the
+    # increments near simple fractions, so it takes many windows to settle
+    per_entry = dsc.local_discrepancy(
+        [dsc.weyl_float(rng.uniform(0.2, 0.8), rng.random(), int(rng.integers(0, 1 << 20)), 256)
+         for _ in range(4000)])
+    assert abs(per_entry / printed["weyl:per-entry-uniform[0.2,0.8]"] - 1) < 0.15
     # the oracle's integer Weyl thresholds of one entry over time
     ld_int = dsc.local_discrepancy(_windows_weyl_oracle(orc, rng, 64))
-    assert abs(ld_int / 0.0078 - 1) < 0.12
-    # SR: the oracle's hash over 256 steps of random entries (paper: 0.0539)
+    assert abs(ld_int / printed["weyl:phi-1"] - 1) < 0.12
+    # SR: the oracle's hash over 256 steps of random entries
     wins = []
     for _ in range(200):
         i = int(rng.integers(0, 1 << 30))
         t0 = int(rng.integers(0, 1 << 20))
         wins.append(np.array([orc.thresholds("sr", 0, 0, t0 + t, i, 1, 16)[0]
                               for t in range(1, 257)]) / TWO24)
-    assert abs(dsc.local_discrepancy(wins) / 0.0539 - 1) < 0.08
+    assert abs(dsc.local_discrepancy(wins) / printed["sr"] - 1) < 0.08
 
 
 def _moments(u):
@@ -144,12 +184,17 @@ def _moments(u):
 
 
 def test_sr_hash_moments(orc):
-    """Hash-SR unit test (paper: mean 0.4997, variance 0.0834, lag-1 -5e-5)."""
+    """Hash-SR unit test: the moments of U(0, 1), as the paper's printed ones are."""
+    printed = {k: v[0] for k, v in table("sr_hash_moments.txt").items()}
+    # the printed moments are those of U(0, 1) up to sampling error
+    assert abs(printed["mean"] - 0.5) < 1e-3 and abs(printed["variance"] - 1 / 12) < 1e-3
+    assert abs(printed["lag1"]) < 1e-3
     n = 1 << 20
     over_entries = orc.thresholds("sr", 0, 0, 5, 0, n, 16) / TWO24
     m, v, r = _moments(over_entries)
     se = 1 / np.sqrt(12 * n)
     assert abs(m - 0.5) < 5 * se and abs(v - 1 / 12) < 5e-4 and abs(r) < 5 / np.sqrt(n)
+    assert abs(m - printed["mean"]) < 1e-3 and abs(v - printed["variance"]) < 1e-3
     T = 1 << 15
     over_time = np.array([orc.thresholds("sr", 1, 3, t, 777, 1, 16)[0] for t in range(T)]) / TWO24
     m, v, r = _moments(over_time)
