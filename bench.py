@@ -63,6 +63,9 @@ def parse_args():
     ap.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                     help="turn rocprofv3 CSV output (kernel trace with --stats, then --pmc "
                          "FETCH_SIZE, then --pmc WRITE_SIZE) into the summaries under profiles/")
+    ap.add_argument("--summarize-valu", metavar="PMC_DIR",
+                    help="turn a rocprofv3 --pmc run of SQ_WAVES, SQ_INSTS_VALU, "
+                         "SQ_ACTIVE_INST_VALU and GRBM_GUI_ACTIVE into profiles/...valu.md")
     return ap.parse_args()
 
 
@@ -88,6 +91,8 @@ def main() -> int:
         args.workload = "m1_long" if args.state_error else "hybrid_m2_stack"
     if args.summarize_profiles:
         return summarize_profiles(args.workload, *args.summarize_profiles)
+    if args.summarize_valu:
+        return summarize_valu(args.workload, args.summarize_valu)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build measures one GPU only; the state update shards "
@@ -523,6 +528,10 @@ def _variant_of(kernel_name: str):
     return f"{f}:{r}"
 
 
+def _short_kernel(name: str) -> str:
+    return name.replace("void ", "").replace("(ssmq::UpdateArgs)", "").replace("ssmq::", "")
+
+
 def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str) -> int:
     """Write profiles/k_update_slab.<workload>.{kernel_trace.md,traffic.md,traffic.json}.
 
@@ -570,7 +579,7 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
         wk = statistics.mean(write.get((k, g), [float("nan")]))
         traffic = fk * 1024.0 * f_fetch + wk * 1024.0 * f_write
         variants[key] = {
-            "kernel": k.replace("void ", "").replace("(ssmq::UpdateArgs)", "").replace("ssmq::", ""),
+            "kernel": _short_kernel(k),
             "dispatches": len(v), "fetch_KiB": fk, "write_KiB": wk,
             "traffic_bytes": traffic, "algorithmic_bytes": algo,
             "traffic_over_algorithmic": traffic / algo,
@@ -619,6 +628,44 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
     return 0
 
 
+def summarize_valu(workload: str, pmc_dir: str) -> int:
+    """Write profiles/k_update_slab.<workload>.valu.md: per variant, VALU
+    instructions per wave and per entry (lane operations), and the VALU busy
+    fraction SQ_ACTIVE_INST_VALU * 4 / SIMDs / (GRBM_GUI_ACTIVE / XCDs)."""
+    import statistics
+    from collections import defaultdict
+
+    from paper_2609_39185_amd import workloads as wl
+
+    w = wl.WORKLOADS[workload]
+    agent = [r for r in _csv_rows(pmc_dir, "agent_info.csv") if r.get("Agent_Type") == "GPU"][0]
+    simds, xcc = int(agent["Simd_Count"]), int(agent["Num_Xcc"])
+    vals = defaultdict(lambda: defaultdict(list))
+    for r in _csv_rows(pmc_dir, "counter_collection.csv"):
+        if _variant_of(r["Kernel_Name"]) is not None:
+            vals[r["Kernel_Name"]][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    rows = []
+    for k, c in vals.items():
+        m = {n: statistics.mean(v) for n, v in c.items()}
+        busy = m["SQ_ACTIVE_INST_VALU"] * 4 / simds / (m["GRBM_GUI_ACTIVE"] / xcc)
+        rows.append((_variant_of(k), _short_kernel(k), m["SQ_INSTS_VALU"] / m["SQ_WAVES"],
+                     m["SQ_INSTS_VALU"] * 64 / w.entries_per_layer, busy, len(c["SQ_WAVES"])))
+    lines = [f"# k_update_slab on {workload}: vector-instruction budget per launch", "",
+             "Command (repository root as $R, run from /tmp with TMPDIR=/tmp):", "",
+             f"    {PROFILE_COMMANDS['valu']}", f"    {PROFILE_COMMANDS['valu_summary']}", "",
+             f"Lane operations per entry = SQ_INSTS_VALU x 64 / {w.entries_per_layer} entries; "
+             f"VALU busy = SQ_ACTIVE_INST_VALU x 4 / {simds} SIMDs / (GRBM_GUI_ACTIVE / {xcc} XCDs).",
+             "", "| variant | kernel | VALU instr per wave | lane ops per entry | VALU busy | dispatches |",
+             "|---|---|---|---|---|---|"]
+    for v, k, per_wave, per_entry, busy, n in sorted(rows):
+        lines.append(f"| {v} | `{k}` | {per_wave:.0f} | {per_entry:.1f} | {100 * busy:.0f} % | {n} |")
+    os.makedirs(PROFILE_DIR, exist_ok=True)
+    with open(os.path.join(PROFILE_DIR, f"k_update_slab.{workload}.valu.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 PROFILE_COMMANDS = {
     "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof_trace "
              "-o run -- python3 $R/bench.py",
@@ -630,6 +677,11 @@ PROFILE_COMMANDS = {
              "--cpu-seconds 0",
     "summary": "python3 $R/bench.py --summarize-profiles $R/gpurun_out/prof_trace "
                "$R/gpurun_out/prof_fetch $R/gpurun_out/prof_write",
+    "valu": "timeout -s KILL 120 rocprofv3 --pmc SQ_WAVES SQ_ACTIVE_INST_VALU SQ_WAVE_CYCLES "
+            "SQ_BUSY_CYCLES SQ_INSTS_VALU GRBM_GUI_ACTIVE --output-format csv "
+            "-d $R/gpurun_out/pmc_busy -o run -- python3 $R/bench.py --steps 2 --warmup 0 "
+            "--layers 4 --cpu-seconds 0 --no-ceiling",
+    "valu_summary": "python3 $R/bench.py --summarize-valu $R/gpurun_out/pmc_busy",
 }
 
 

@@ -198,9 +198,10 @@ ssmq_status ssmq_state_update_ex(const ssmq_dims* dims, const ssmq_qparams* q,
                 "with SSMQ_FLAG_FP32_STATE scale groups must be powers of two up to 1024 entries");
 
   // Slab kernels for per-head A: a workgroup owns whole rows of one head, two
-  // 16-byte chunks per thread; with one scale per head (scaled formats) the workgroup owns
-  // the whole head, four chunks per thread (fewer, fuller threads amortise the
-  // per-workgroup scale reduction and its barriers).
+  // chunks per thread (the whole head when it holds 1024 chunks or a multiple:
+  // one decay and one B/C staging per head); with one scale per head (scaled
+  // formats) the workgroup owns the whole head, four chunks per thread (fewer,
+  // fuller threads amortise the per-workgroup scale reduction and its barriers).
   int cfg = -1;
   const int64_t head_chunks = head_size / V;
   if (d.a_per_state == 0 && scaled && group == head_size && !fp32_state) {
@@ -216,7 +217,9 @@ ssmq_status ssmq_state_update_ex(const ssmq_dims* dims, const ssmq_qparams* q,
     if (cfg >= 0) { a.slabs_per_head = 1; a.lanes_per_group = 0; }
   }
   if (cfg < 0 && d.a_per_state == 0 && small_groups_ok && head_chunks % 256 == 0 && !fp32_state) {
-    cfg = (head_chunks % 512 == 0) ? ssmq::kSlab256x2 : ssmq::kSlab256x1;
+    cfg = (head_chunks % 1024 == 0) ? ssmq::kSlab512x2
+          : (head_chunks % 512 == 0)  ? ssmq::kSlab256x2
+                                      : ssmq::kSlab256x1;
     a.slabs_per_head = static_cast<int32_t>(
         head_chunks / (ssmq::kSlabThreads[cfg] * ssmq::kSlabChunks[cfg]));
     a.lanes_per_group = scaled ? static_cast<int32_t>(group / 16) : 1;

@@ -94,6 +94,11 @@ void k_update_slab(UpdateArgs a) {
   // exp(dt A), evaluated by the first wave in double with one final rounding.
   __shared__ float4 sBC[kMaxDstate / 2];
   __shared__ float sh[3];
+  // y of the slab is staged here and written back as whole lines (the integer
+  // formats, whose kernels measure 2-3 % slower that way, store it directly).
+  constexpr bool kStageY = !(F == kINT8 || F == kINT4);
+  __shared__ float sY[kStageY ? NT * CPT : 1];
+  __shared__ uint32_t sDone;  // waves whose rows of y are in sY
   const int nq = a.dstate >> 2;  // float4 per vector
   const float* Bg = a.B + (b * a.ngroups + g) * a.dstate;
   const float* Cg = a.C + (b * a.ngroups + g) * a.dstate;
@@ -103,7 +108,7 @@ void k_update_slab(UpdateArgs a) {
   if (t < 64) {
     const float dte = step_size(a, dt_in, hh);
     const float d = decay(dte, a.A[hh]);
-    if (t == 0) { sh[0] = d; sh[2] = dte; }
+    if (t == 0) { sh[0] = d; sh[2] = dte; sDone = 0; }
   }
   __syncthreads();
   const float dA = sh[0];
@@ -141,9 +146,13 @@ void k_update_slab(UpdateArgs a) {
     bad[j] = !__builtin_isfinite(ys);
     ys = lane_sum(ys, a.lanes_per_row);
     if (cc == 0) {
-      float yv = ys + Dv * xv[j];
-      if (a.z) yv = yv * silu(a.z[tile * a.headdim + r0 + j * rows_per_pass]);
-      hy[r0 + j * rows_per_pass] = yv;
+      if constexpr (kStageY) {
+        sY[(t >> a.lr_shift) + j * rows_per_pass] = ys + Dv * xv[j];
+      } else {
+        float yv = ys + Dv * xv[j];
+        if (a.z) yv = yv * silu(a.z[tile * a.headdim + r0 + j * rows_per_pass]);
+        hy[r0 + j * rows_per_pass] = yv;
+      }
     }
   }
 
@@ -205,6 +214,25 @@ void k_update_slab(UpdateArgs a) {
         h[j], r[j], chunk_thr<R, V>(a.entry_base + static_cast<uint64_t>(e), a.thr, base, a.toff),
         bad[j]);
     store_stream(hstate + chunk_bytes_at<F>(l0 + j * pass), out);
+  }
+
+  // y leaves as whole lines rather than one float per row from every wave: each
+  // wave counts itself in after its rows are in sY, and the last one to arrive
+  // writes the slab's rows (the others exit; nothing waits).
+  if constexpr (!kStageY) return;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  uint32_t arrived = 0;
+  if ((t & 63) == 0) arrived = atomicAdd(&sDone, 1u);
+  arrived = __shfl(arrived, 0);
+  if (arrived == NW - 1) {
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    const int rows_slab = rows_per_pass * CPT;
+    const int row0 = static_cast<int>(slab) * rows_slab;
+    for (int i = t & 63; i < rows_slab; i += 64) {
+      float yv = sY[i];
+      if (a.z) yv = yv * silu(a.z[tile * a.headdim + row0 + i]);
+      hy[row0 + i] = yv;
+    }
   }
 }
 

@@ -284,18 +284,22 @@ def test_proposition1_through_the_kernel(ssmq):
 # full-size workloads, sampled tiles against the oracle
 # --------------------------------------------------------------------------
 def _full_size_sampled(ssmq, name, fmt, rule, n_tiles=24):
+    """One full-size layer in the launch configuration the bench times; sampled head
+    tiles against the oracle (codes within the bar, scales exact, y within 1e-5)."""
     import paper_2609_39185_amd as m
     w = wl.WORKLOADS[name]
     b, H, P, N, G = w.batch, w.nheads, w.headdim, w.dstate, w.ngroups
-    say(f"case full size {name} {fmt} {rule}: {w.entries_per_layer} entries")
+    grp = wl.scale_group_of(w, fmt)
+    per_tile = (P * N) // (grp or P * N) if fmt in oracle.SCALED else 0
+    say(f"case full size {name} {fmt} {rule} group {grp}: {w.entries_per_layer} entries")
     A, D = wl.layer_params(w.family, H, N, 500, device=DEV)
     x, dt, B, C = wl.step_inputs(b, H, P, N, G, 501, device=DEV)
-    codes, scale = wl.initial_state(fmt, b, H, P, N, 502, device=DEV)
+    codes, scale = wl.initial_state(fmt, b, H, P, N, 502, group=grp, device=DEV)
     before = codes.clone()
     sbefore = None if scale is None else scale.clone()
     y = torch.empty((b, H, P), dtype=torch.float32, device=DEV)
     m.state_update(codes, scale, x, dt, A, B, C, D, y, rule=rule, fmt=fmt,
-                   dither_block=w.dither_block, step=777, layer=5)
+                   dither_block=w.dither_block, scale_group=grp, step=777, layer=5)
     torch.cuda.synchronize()
     rng = np.random.default_rng(0)
     tiles = rng.choice(b * H, size=n_tiles, replace=False)
@@ -305,28 +309,33 @@ def _full_size_sampled(ssmq, name, fmt, rule, n_tiles=24):
         bb, hh = divmod(int(tile), H)
         gg = hh // hpg
         cs = lambda t: t.detach().cpu()
+        sl = slice(tile * per_tile, (tile + 1) * per_tile) if per_tile else None
         r_codes, r_scale, r_y, r_h = oracle.state_update(
             fmt, rule, wl.to_numpy_codes(fmt, cs(before[bb:bb + 1, hh:hh + 1])),
-            None if sbefore is None else cs(sbefore[tile:tile + 1]).numpy(),
+            None if sbefore is None else cs(sbefore[sl]).numpy(),
             cs(x[bb:bb + 1, hh:hh + 1]).numpy(), cs(dt[bb:bb + 1, hh:hh + 1]).numpy(),
             cs(A[hh:hh + 1]).numpy(), cs(B[bb:bb + 1, gg:gg + 1]).numpy(),
             cs(C[bb:bb + 1, gg:gg + 1]).numpy(), cs(D[hh:hh + 1]).numpy(),
-            step=777, layer=5, block=w.dither_block, entry_base=int(tile) * P * N)
+            step=777, layer=5, block=w.dither_block, group=grp, entry_base=int(tile) * P * N)
         got = wl.to_numpy_codes(fmt, cs(codes[bb:bb + 1, hh:hh + 1]))
         from ._parity import code_stats
         nd, ulp = code_stats(fmt, got, r_codes)
         assert nd <= 1 and ulp <= 1, (tile, nd, ulp)
         if scale is not None:
-            assert np.array_equal(cs(scale[tile:tile + 1]).numpy(), r_scale)
+            assert np.array_equal(cs(scale[sl]).numpy(), r_scale)
         Ch = cs(C[bb, gg]).numpy().astype(np.float64)
         mag = np.abs(Ch[None, :] * r_h[0, 0]).sum(-1) + abs(float(D[hh]) * cs(x[bb, hh]).numpy())
         yg = cs(y[bb, hh]).numpy().astype(np.float64)
         assert np.all(np.abs(yg - r_y[0, 0]) <= 1e-5 * (mag + np.abs(r_y[0, 0])))
 
 
-@pytest.mark.parametrize("fmt,rule", [("bf16", "weyl"), ("bf16", "sr"), ("e4m3", "weyl"),
-                                      ("e4m3", "rtn")])
+BENCH_VARIANTS = [(f, r) for f in ("bf16", "e4m3", "int8") for r in ("weyl", "sr", "rtn", "philox")]
+BENCH_VARIANTS += [("int4", r) for r in ("weyl", "sr", "rtn")]
+
+
+@pytest.mark.parametrize("fmt,rule", BENCH_VARIANTS)
 def test_full_size_hybrid_stack_layer(ssmq, fmt, rule):
+    """Every format and rule the bench reports, at the bench's layer shape."""
     _full_size_sampled(ssmq, "hybrid_m2_stack", fmt, rule)
 
 
