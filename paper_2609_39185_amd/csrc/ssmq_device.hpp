@@ -381,10 +381,11 @@ __device__ inline bool chunk_has_nan(const float (&v)[V]) {
 // the group maximum to 448): the stochastic conversions, which do not saturate,
 // get values clamped with v_med3_f32 (clamping first is eq. (dither) on the
 // saturated grid); round-to-nearest needs no clamp below 464, which a scaled
-// value never reaches.
+// value never reaches. clamp = false (wave-uniform): the caller knows that no
+// value of the group exceeds 448 (fl32(max|h| r) <= 448; rounding is monotonic).
 template <int F, int R, typename TG>
 __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG& tg,
-                                       bool maybe_nan) {
+                                       bool maybe_nan, bool clamp = true) {
   constexpr int V = Traits<F>::V;
   uint32_t w[4];
   if constexpr (F == kFP32) {
@@ -425,8 +426,11 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG&
   } else {  // E4M3, values already scaled
     float q[V];
 #pragma unroll
-    for (int k = 0; k < V; ++k)
-      q[k] = (R == kRTN) ? v[k] : __builtin_amdgcn_fmed3f(v[k], -448.0f, 448.0f);
+    for (int k = 0; k < V; ++k) q[k] = v[k];
+    if (R != kRTN && clamp) {
+#pragma unroll
+      for (int k = 0; k < V; ++k) q[k] = __builtin_amdgcn_fmed3f(v[k], -448.0f, 448.0f);
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int k = 4 * i;
@@ -528,14 +532,14 @@ __device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, f
 // chunk's group (ignored by unscaled formats).
 template <int F, int R, typename TG>
 __device__ inline chunk_t<F> quantize_any(const float (&h)[Traits<F>::V], float r, const TG& tg,
-                                         bool maybe_nan) {
+                                         bool maybe_nan, bool clamp = true) {
   if constexpr (is_int_fmt<F>) {
     return quantize_int_chunk<F, R>(h, r, r * 0x1p24f, tg, maybe_nan);
   } else if constexpr (F == kE4M3) {
     float v[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k) v[k] = h[k] * r;
-    return quantize_chunk<F, R>(v, tg, maybe_nan);
+    return quantize_chunk<F, R>(v, tg, maybe_nan, clamp);
   } else {
     return quantize_chunk<F, R>(h, tg, maybe_nan);
   }

@@ -93,7 +93,7 @@ void k_update_slab(UpdateArgs a) {
   // are in flight: B and C of the head's group (one float4 per thread), and
   // exp(dt A), evaluated by the first wave in double with one final rounding.
   __shared__ float4 sBC[kMaxDstate / 2];
-  __shared__ float sh[3];
+  __shared__ float sh[4];
   // y of the slab is staged here and written back as whole lines (the integer
   // formats, whose kernels measure 2-3 % slower that way, store it directly).
   constexpr bool kStageY = !(F == kINT8 || F == kINT4);
@@ -157,6 +157,7 @@ void k_update_slab(UpdateArgs a) {
   }
 
   float r[CPT];  // scaled formats: 1 / s of each chunk's group
+  bool clamp = true;  // E4M3 dithers: some value may exceed 448 after scaling
 #pragma unroll
   for (int j = 0; j < CPT; ++j) r[j] = 1.0f;
   if constexpr (Traits<F>::scaled) {
@@ -183,14 +184,19 @@ void k_update_slab(UpdateArgs a) {
 #pragma unroll
         for (int i = 1; i < NW; ++i) w = max(w, red[i]);
         const float s = group_scale<F>(__uint_as_float(w));
+        const float rs = recip_scale(s);
         if (t == 0) {
           sh[0] = s;
-          sh[1] = recip_scale(s);
+          sh[1] = rs;
+          sh[3] = (__uint_as_float(w) * rs <= 448.0f) ? 0.0f : 1.0f;  // E4M3: clamp needed
           a.scale[tile] = s;
         }
       }
       __syncthreads();
       const float rs = sh[1];
+      // A per-head scale whose own rounding leaves max|h| r <= 448 (about four
+      // heads in five) needs the E4M3 clamp nowhere in the head.
+      clamp = __builtin_amdgcn_readfirstlane(__float_as_uint(sh[3])) != 0u;
 #pragma unroll
       for (int j = 0; j < CPT; ++j) r[j] = rs;
     } else {  // groups of lanes_per_group consecutive lanes of one pass
@@ -212,7 +218,7 @@ void k_update_slab(UpdateArgs a) {
                                            : thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr));
     const chunk_t<F> out = quantize_any<F, R>(
         h[j], r[j], chunk_thr<R, V>(a.entry_base + static_cast<uint64_t>(e), a.thr, base, a.toff),
-        bad[j]);
+        bad[j], clamp);
     store_stream(hstate + chunk_bytes_at<F>(l0 + j * pass), out);
   }
 
