@@ -560,8 +560,8 @@ int orc_requantize(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step
  */
 /*
  * The decode-step operations on either side of the update, as in the Mamba
- * reference implementation the paper's runners follow (Appendix B "Runners":
- * "conv and gating exactly as in the reference"):
+ * reference implementation the paper's runners follow for the convolution and
+ * the gate (Appendix B "Runners"):
  *   step size   dt' = softplus(fl32(dt + dt_bias)), softplus(v) = log(1 + e^v)
  *               evaluated in double and rounded once (v itself above 20, where
  *               the two agree in fp32);

@@ -367,3 +367,64 @@ def test_errors(ssmq):
     assert e.value.status == 1
     with pytest.raises(ValueError):
         m.state_update(st.cpu(), None, x, dt, A, B, B, None, y, rule="weyl", fmt="bf16")
+
+
+# --------------------------------------------------------------------------
+# E4M3 with one scale per head: the saturating clamp, and when it may be skipped
+# --------------------------------------------------------------------------
+def _scale_with_overshoot(over):
+    """An old scale s0 for which a head whose maximum is the code 448 gets, after
+    h = 448 s0 and the new scale s = fl32(h / 448), r = fl32(1 / s), a scaled
+    maximum q = fl32(h r) of 448 + `over` fp32 ulps (over <= 0: at most 448)."""
+    rng = np.random.default_rng(11)
+    for _ in range(200000):
+        s0 = np.float32(rng.uniform(1, 2) * 2.0 ** int(rng.integers(-12, 12)))
+        m = np.float32(np.float32(448) * s0)
+        s = np.float32(m / np.float32(448))
+        q = np.float32(m * np.float32(np.float32(1) / s))
+        if int(q.view(np.uint32)) - 0x43E00000 == over:
+            return s0
+    raise AssertionError(f"no scale found with overshoot {over}")
+
+
+@pytest.mark.parametrize("rule", ["weyl", "sr"])
+@pytest.mark.parametrize("over", [1, 0, -1])
+def test_e4m3_head_scale_overshoot_saturates(ssmq, rule, over):
+    """dt = 0 keeps h = 448 s0 at one entry and 0 elsewhere. When the scaled maximum
+    passes 448 its threshold is chosen (from the oracle's generator) so that an
+    unsaturated stochastic conversion would carry into the NaN code; the stored
+    code must be 448 (0x7E), as the oracle's clamp gives, and every code and the
+    scale must equal the oracle's. Without overshoot the clamp is skipped."""
+    import paper_2609_39185_amd as m
+    P, N = 64, 128
+    s0 = _scale_with_overshoot(over)
+    need = (1 << 24) - 16 * max(over, 1)  # carry past 448: over + (U >> 4) >= 2^20
+    entry = step = None
+    for t in range(1, 40000):
+        U = oracle.thresholds(rule, 0, 2, t, 0, P * N, 128)
+        hit = np.nonzero(U >= need)[0]
+        if hit.size:
+            entry, step = int(hit[0]), t
+            break
+    assert entry is not None
+    say(f"case e4m3 {rule} overshoot {over}: entry {entry} step {step} s0 {float(s0)!r}")
+    codes = torch.zeros((1, 1, P, N), dtype=torch.uint8)
+    codes.view(-1)[entry] = 0x7E
+    scale = torch.tensor([s0], dtype=torch.float32)
+    x = torch.zeros((1, 1, P))
+    dt = torch.zeros((1, 1))
+    A = torch.tensor([-1.5])
+    B = torch.randn((1, 1, N), generator=torch.Generator().manual_seed(3))
+    C = torch.randn((1, 1, N), generator=torch.Generator().manual_seed(4))
+    st, sc = codes.to(DEV), scale.to(DEV)
+    y = torch.empty((1, 1, P), device=DEV)
+    m.state_update(st, sc, x.to(DEV), dt.to(DEV), A.to(DEV), B.to(DEV), C.to(DEV), None, y,
+                   rule=rule, fmt="e4m3", dither_block=128, layer=2, step=step)
+    torch.cuda.synchronize()
+    r_codes, r_scale, _, _ = oracle.state_update(
+        "e4m3", rule, codes.numpy(), scale.numpy(), x.numpy(), dt.numpy(), A.numpy(), B.numpy(),
+        C.numpy(), np.zeros(1, np.float32), layer=2, step=step, block=128)
+    got = st.cpu().numpy()
+    assert r_codes.ravel()[entry] == 0x7E and np.count_nonzero(r_codes) == 1
+    assert np.array_equal(got, r_codes), (got.ravel()[entry], r_codes.ravel()[entry])
+    assert np.array_equal(sc.cpu().numpy(), r_scale)
