@@ -103,6 +103,9 @@ def lib() -> ctypes.CDLL:
     L.orc_state_update_ex.restype = _int
     L.orc_conv1d_update.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, _vp, _int, _vp]
     L.orc_conv1d_update.restype = _int
+    L.orc_replay.argtypes = [_int, _int, _u32, _u32, _u32, _u64, _u64, _i64, _i64, _i64, _i64,
+                             _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+    L.orc_replay.restype = _int
     _lib = L
     return L
 
@@ -288,3 +291,33 @@ def dequantize(fmt: str, codes, scale=None, group=0) -> np.ndarray:
         s = np.repeat(np.asarray(scale, np.float32).ravel(), group)
         v = (v * s).astype(np.float32)
     return v.reshape(shape)
+
+
+def replay(fmt: str, rule: str, h0, a, w, *, seed=0, layer=0, step=0, entry_base=0, block=16,
+           group=0, block_steps=None):
+    """Open-loop replay of traces a, w [T, n] from the FP32 state h0 [n] (Appendix B
+    "Open-loop replay"). Returns a dict: err and ref [n_blocks, n] (float64 sums of
+    (hq_t - h_t)^2 and h_t^2 per block of block_steps steps), codes and scale of the
+    final stored state, and h_final (the final FP32 reference state)."""
+    h0 = _c(h0, np.float32).ravel()
+    n = h0.size
+    a = _c(a, np.float32).reshape(-1, n)
+    w = _c(w, np.float32).reshape(-1, n)
+    steps = a.shape[0]
+    if w.shape[0] != steps:
+        raise ValueError("a and w must hold the same number of steps")
+    bs = block_steps or max(steps, 1)
+    n_blocks = (steps + bs - 1) // bs
+    err = np.zeros((n_blocks, n), np.float64)
+    ref = np.zeros((n_blocks, n), np.float64)
+    per = entries_per_code_word(fmt)
+    codes = np.zeros((n + per - 1) // per, CODE_DTYPE[fmt])
+    scale = np.zeros(n // group, np.float32) if fmt in SCALED and group else None
+    h_final = np.zeros(n, np.float32)
+    rc = lib().orc_replay(FORMATS[fmt], RULES[rule], seed & 0xFFFFFFFF, layer & 0xFFFFFFFF,
+                          step & 0xFFFFFFFF, entry_base, block, n, group, steps, bs, _ptr(h0),
+                          _ptr(a), _ptr(w), _ptr(err), _ptr(ref), _ptr(codes), _ptr(scale),
+                          _ptr(h_final))
+    if rc != 0:
+        raise ValueError("oracle replay rejected its arguments")
+    return {"err": err, "ref": ref, "codes": codes, "scale": scale, "h_final": h_final}

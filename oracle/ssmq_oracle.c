@@ -732,3 +732,79 @@ int orc_conv1d_update(int64_t batch, int64_t channels, int64_t width, float *sta
     }
     return 0;
 }
+
+/*
+ * Open-loop replay (Appendix B "Open-loop replay"; Section 6.2, the paragraph on
+ * the recurrence alone): each entry i of a recorded trace carries its decays
+ * a_t[i] and writes w_t[i], t = 1..T, and its FP32 state h_0[i] at the end of
+ * prefill. Two trajectories are iterated side by side:
+ *   reference  h_t  = fma(a_t, h_{t-1}, w_t)                     (fp32)
+ *   stored     hq_0 = Q_0(h_0),   hq_t = Q_t(fma(a_t, hq_{t-1}, w_t))
+ * Q_t requantizes the whole vector under (rule, format) with the thresholds of
+ * global index entry_base + i and step step0 + t (orc_requantize, group scales
+ * for E4M3/INT8/INT4), and returns the stored value: the code's value, times
+ * its group scale in fp32 for the scaled formats. Per block k of block_steps
+ * steps (steps k*block_steps + 1 .. (k+1)*block_steps; the last may be shorter)
+ *   err[k][i] = sum (hq_t - h_t)^2,   ref[k][i] = sum h_t^2,
+ * each term formed and added in double, in step order. Optional outputs (NULL
+ * to skip): codes and scales of hq_T, and h_T.
+ * Layout: a and w are [T][n]; err and ref are [ceil(T / block_steps)][n].
+ * Returns 0, or -1 on bad arguments.
+ */
+int orc_replay(int f, int rule, uint32_t seed, uint32_t layer, uint32_t step0,
+               uint64_t entry_base, uint64_t block, int64_t n, int64_t group, int64_t steps,
+               int64_t block_steps, const float *h0, const float *a, const float *w,
+               double *err, double *ref, void *codes_out, float *scale_out, float *h_final) {
+    ensure_init();
+    if (f < 0 || f >= ORC_NFMT || n < 0 || steps < 0 || block_steps < 1 || block == 0) return -1;
+    if (is_scaled(f) && (group <= 0 || n % group != 0)) return -1;
+    const int64_t n_alloc = n > 0 ? n : 1;
+    float *x = (float *)malloc(sizeof(float) * (size_t)n_alloc);
+    float *hq = (float *)malloc(sizeof(float) * (size_t)n_alloc);
+    float *href = (float *)malloc(sizeof(float) * (size_t)n_alloc);
+    void *codes = calloc((size_t)n_alloc, 4);
+    float *sc = is_scaled(f) ? (float *)calloc((size_t)(n_alloc / group + 1), sizeof(float)) : NULL;
+    int rc = 0;
+    for (int64_t t = 0; t <= steps && rc == 0; ++t) {
+        for (int64_t i = 0; i < n; ++i) {
+            if (t == 0) {
+                href[i] = h0[i];
+                x[i] = h0[i];
+            } else {
+                const float at = a[(t - 1) * n + i], wt = w[(t - 1) * n + i];
+                href[i] = fmaf(at, href[i], wt);
+                x[i] = fmaf(at, hq[i], wt);
+            }
+        }
+        rc = orc_requantize(f, rule, seed, layer, step0 + (uint32_t)t, entry_base, block, n, group,
+                            x, codes, sc);
+        if (rc != 0) break;
+        for (int64_t i = 0; i < n; ++i) {
+            const float v = code_value(f, load_code(f, codes, i));
+            hq[i] = is_scaled(f) ? v * sc[i / group] : v;
+        }
+        if (t == 0) continue;
+        const int64_t k = (t - 1) / block_steps;
+        for (int64_t i = 0; i < n; ++i) {
+            if ((t - 1) % block_steps == 0) {
+                err[k * n + i] = 0.0;
+                if (ref) ref[k * n + i] = 0.0;
+            }
+            const double d = (double)hq[i] - (double)href[i];
+            err[k * n + i] += d * d;
+            if (ref) ref[k * n + i] += (double)href[i] * (double)href[i];
+        }
+    }
+    if (rc == 0) {
+        if (codes_out) memcpy(codes_out, codes, f == ORC_INT4 ? (size_t)((n + 1) / 2)
+                                                              : (size_t)(n * code_bytes(f)));
+        if (scale_out && sc) memcpy(scale_out, sc, sizeof(float) * (size_t)(n / group));
+        if (h_final) memcpy(h_final, href, sizeof(float) * (size_t)n);
+    }
+    free(x);
+    free(hq);
+    free(href);
+    free(codes);
+    free(sc);
+    return rc;
+}
