@@ -50,6 +50,12 @@ def parse_args():
                     help="--state-error: decay-rate recipe")
     ap.add_argument("--se-cc", type=int, default=0,
                     help="--state-error: also run checkpointed rules, rounding every k-th write")
+    ap.add_argument("--replay", action="store_true",
+                    help="instead of throughput: open-loop replay of synthetic recorded traces")
+    ap.add_argument("--rp-batch", type=int, default=0,
+                    help="--replay: sequences in the traced layer (0 = the workload's batch)")
+    ap.add_argument("--rp-memory", default="trained", choices=("short", "trained"),
+                    help="--replay: decay-rate recipe")
     ap.add_argument("--variants", default="bf16:weyl,bf16:sr,bf16:rtn,bf16:philox,"
                                           "e4m3:weyl,e4m3:sr,e4m3:rtn,e4m3:philox,"
                                           "int8:weyl,int8:sr,int8:rtn,int8:philox,"
@@ -88,7 +94,7 @@ def state_bytes_per_launch(w, fmt: str) -> int:
 def main() -> int:
     args = parse_args()
     if args.workload is None:
-        args.workload = "m1_long" if args.state_error else "hybrid_m2_stack"
+        args.workload = "m1_long" if (args.state_error or args.replay) else "hybrid_m2_stack"
     if args.summarize_profiles:
         return summarize_profiles(args.workload, *args.summarize_profiles)
     if args.summarize_valu:
@@ -107,6 +113,11 @@ def main() -> int:
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = wl.WORKLOADS[args.workload]
+    if args.replay:
+        res = replay_study(w, steps=args.steps or 2048, batch=args.rp_batch or w.batch,
+                           block=args.block, memory=args.rp_memory, device=dev)
+        print(json.dumps(res), flush=True)
+        return 0
     if args.state_error:
         res = state_error_study(w, steps=args.steps or w.steps, layers=args.layers or w.layers,
                                 block=args.block, device=dev, fmt=args.se_format,
@@ -297,6 +308,119 @@ def decode_state(fmt: str, codes, scale, group: int):
         v = torch.stack(((lo ^ 8) - 8, (hi ^ 8) - 8), dim=-1).flatten(-2).float()
     flat = v.reshape(-1, group) * scale.reshape(-1, 1)
     return flat.reshape(v.shape)
+
+
+REPLAY_FORMATS = (("fp16", 0), ("bf16", 0), ("int8", 16), ("int4", 16), ("e4m3", 16))
+REPLAY_RULES = (("rtn", 0), ("sr", 0), ("sr", 1), ("weyl", 0), ("philox", 0))
+TAU_LABELS = ("<10", "10-100", "100-1000", ">=1000")
+
+
+def replay_study(w, *, steps: int, batch: int, block: int, memory: str, device, warmup: int = 128,
+                 formats=REPLAY_FORMATS, rules=REPLAY_RULES) -> dict:
+    """Open-loop replay (Appendix B "Open-loop replay"; Section 6.2): the rounding
+    error of the state recurrence alone, on recorded per-entry decays and writes.
+
+    One Mamba-1 layer of workload w ([batch][d_inner][N] entries, dither block 16)
+    is run in FP32 for `warmup` steps (the prefill, from a zero state); the state
+    then is h0, and the next `steps` steps are recorded as traces a_t = exp(dt A)
+    and w_t = dt x B ([steps][n] each, resident in HBM). Step t draws dt, x and B
+    from a generator seeded with splitmix64(5000, t). ssmq_replay then replays the
+    traces for every (format, rule), starting from the quantized h0 (step 0), and
+    the error sum (hq_t - h_t)^2 / sum h_t^2 is reported over the whole replay,
+    per block of `block` steps, and per memory bin tau = 1 / (1 - exp(A dt_bar)),
+    dt_bar the channel's mean step size over the recorded steps and sequences.
+    Each replay launch is timed with events: trace bytes (8 per entry and step)
+    over its duration.
+    """
+    import torch
+
+    import paper_2609_39185_amd as ssmq
+    from paper_2609_39185_amd import workloads as wl
+
+    if w.family != "mamba1":
+        raise ValueError("the replay study is defined on the Mamba-1 shapes")
+    b, d, N = batch, w.nheads, w.dstate
+    n = b * d * N
+    params = wl.layer_params if memory == "short" else wl.layer_params_trained_memory
+    A, _ = params(w.family, d, N, seed=1000, device=device)              # [d, N]
+    a_tr = torch.empty((steps, n), dtype=torch.float32, device=device)
+    w_tr = torch.empty((steps, n), dtype=torch.float32, device=device)
+    h = torch.zeros((b, d, N), dtype=torch.float32, device=device)
+    dt_sum = torch.zeros(d, dtype=torch.float64, device=device)
+    t0 = time.perf_counter()
+    for t in range(1 - warmup, steps + 1):
+        gen = torch.Generator(device=device)
+        gen.manual_seed(wl.splitmix64(5000, t + warmup))
+        dt = torch.nn.functional.softplus(torch.randn((b, d), generator=gen, device=device) - 4.0)
+        x = torch.randn((b, d), generator=gen, device=device)
+        B = torch.randn((b, N), generator=gen, device=device)
+        at = torch.exp(dt[:, :, None] * A[None])                           # [b, d, N]
+        wt = (dt * x)[:, :, None] * B[:, None, :]
+        if t <= 0:
+            h = torch.addcmul(wt, at, h)
+        else:
+            a_tr[t - 1].copy_(at.reshape(-1))
+            w_tr[t - 1].copy_(wt.reshape(-1))
+            dt_sum += dt.double().sum(0)
+    h0 = h.reshape(-1).contiguous()
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - t0
+    dt_bar = (dt_sum / (b * max(steps, 1))).float()
+    tau = 1.0 / (1.0 - torch.exp(A * dt_bar[:, None]))                     # [d, N]
+    bins = torch.bucketize(tau, torch.tensor(TAU_EDGES, device=device))
+    n_bins = len(TAU_EDGES) + 1
+    onehot = torch.nn.functional.one_hot(bins, n_bins).to(torch.float64)   # [d, N, bins]
+    share = torch.bincount(bins.flatten(), minlength=n_bins).double() / bins.numel()
+    nb = (steps + block - 1) // block
+    stream = torch.cuda.current_stream(device)
+    out, timing = {}, {}
+    den_bins = None
+    for fmt, g in formats:
+        res = {}
+        for rule, seed in rules:
+            err = torch.empty((nb, n), dtype=torch.float64, device=device)
+            ref = torch.empty((nb, n), dtype=torch.float64, device=device)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            ssmq.replay(h0, a_tr, w_tr, err, rule=rule, fmt=fmt, ref=ref, block_steps=block,
+                        scale_group=g, dither_block=w.dither_block, seed=seed, layer=0, step=0,
+                        stream=stream)
+            e1.record(stream)
+            e1.synchronize()
+            ms = e0.elapsed_time(e1)
+            name = rule if rule != "sr" else f"sr_seed{seed}"
+            timing[f"{fmt}:{name}"] = ms
+            num = torch.einsum("kdn,dnj->kj", err.view(nb, b, d, N).sum(1), onehot)   # [blocks, bins]
+            den = torch.einsum("kdn,dnj->kj", ref.view(nb, b, d, N).sum(1), onehot)
+            den_bins = den
+            res[name] = {
+                "error": float(num.sum() / den.sum()),
+                "error_per_block": [float(v) for v in num.sum(1) / den.sum(1)],
+                "error_by_tau_bin": {TAU_LABELS[j]: float(num[:, j].sum() / den[:, j].sum())
+                                     for j in range(n_bins) if float(den[:, j].sum()) > 0},
+            }
+            print(f"replay: {fmt} {name} {ms:.2f} ms", file=sys.stderr, flush=True)
+        sr = res["sr_seed0"]
+        for name, r in res.items():
+            r["over_sr_seed0"] = r["error"] / sr["error"]
+            r["over_sr_seed0_by_tau_bin"] = {k: v / sr["error_by_tau_bin"][k]
+                                             for k, v in r["error_by_tau_bin"].items()}
+        out[fmt + (f"_block{g}" if g else "")] = res
+    trace_bytes = 8 * n * steps
+    best = min(timing.values())
+    return {
+        "study": "open_loop_replay",
+        "metric": "relative state error sum((hq-h)^2)/sum(h^2) of the replayed recurrence",
+        "workload": w.name, "batch": b, "d_inner": d, "dstate": N, "entries": n, "steps": steps,
+        "warmup_steps": warmup, "block": block, "dither_block": w.dither_block, "memory": memory,
+        "data": "synthetic traces", "tau_bin_share": dict(zip(TAU_LABELS, [float(v) for v in share])),
+        "results": out,
+        "replay_ms": timing,
+        "replay_trace_GBps_best": trace_bytes / (best * 1e-3) / 1e9,
+        "replay_entry_steps_per_s_best": n * steps / (best * 1e-3),
+        "trace_generation_s": gen_s,
+    }
 
 
 def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: str = "fp16",

@@ -233,6 +233,44 @@ ssmq_status ssmq_dither_fill(int32_t rule, uint32_t seed, uint32_t layer, uint32
                              uint64_t entry_base, int64_t n, int32_t dither_block,
                              uint32_t* U24, void* stream);
 
+/*
+ * ssmq_replay -- open-loop replay of recorded decays and writes under one rule
+ * and format (Appendix B "Open-loop replay"; Section 6.2, on the recurrence
+ * alone reproducing the gain): the error a rounding rule accumulates in the
+ * state recurrence by itself, without the rest of the network.
+ *
+ * Defines, for each entry i of a trace of n entries and T = steps steps:
+ *   reference  h_0 = h0[i],        h_t  = fma(a[t-1][i], h_(t-1), w[t-1][i])   (fp32)
+ *   stored     hq_0 = Q_0(h0[i]),  hq_t = Q_t(fma(a[t-1][i], hq_(t-1), w[t-1][i]))
+ * where Q_t is the write-back of ssmq_requantize under q (rule, format, dither
+ * block, seed, layer, entry_base) at step q->step + t, returning the stored value:
+ * the code's value, times its group scale in fp32 for E4M3, INT8 and INT4 (each
+ * group of q->scale_group consecutive entries gets scale fl32(max|x| / qmax)).
+ * For each block k of block_steps steps (steps k*block_steps + 1 ..
+ * min((k+1)*block_steps, T)):
+ *   err[k][i] = sum (hq_t - h_t)^2      ref[k][i] = sum h_t^2
+ * each term formed in double from the fp32 values and added in step order.
+ * The state error of a set of entries is sum err / sum ref over them.
+ *
+ * Arguments (device pointers; alignment in brackets):
+ *   n            entries, a multiple of 4 (and of the scale group); 0 is a no-op
+ *   steps        T >= 0; block_steps >= 1
+ *   h0           [n] fp32, the state at the end of prefill [16 B]
+ *   a, w         [T][n] fp32 decays and writes [16 B]
+ *   err          [ceil(T / block_steps)][n] double, written [16 B]
+ *   ref          as err, or NULL [16 B]
+ *   codes        [n] codes of hq_T (2 B fp16/bf16, 1 B E4M3 and INT8, 4 B fp32, INT4
+ *                two per byte), or NULL [16 B]
+ *   scale        E4M3, INT8, INT4: [n / scale_group] scales of hq_T, or NULL [4 B]
+ *   h_final      [n] fp32 h_T, or NULL [16 B]
+ * q->scale_group: for the scaled formats a power of two from 4 to 256 entries
+ * (the paper's blocks are 16 and 128); q->flags must be 0; q->entry_base is a
+ * multiple of 16 as everywhere.
+ */
+ssmq_status ssmq_replay(const ssmq_qparams* q, int64_t n, int32_t steps, int32_t block_steps,
+                        const float* h0, const float* a, const float* w, double* err, double* ref,
+                        void* codes, float* scale, float* h_final, void* stream);
+
 /* Static text for a status code. Never NULL. */
 const char* ssmq_status_string(ssmq_status s);
 

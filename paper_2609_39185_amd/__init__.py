@@ -7,10 +7,11 @@ by round-to-nearest, stochastic rounding or the golden-ratio Weyl dither
 is the thin Python binding (argument marshalling) plus seeded workloads.
 """
 from ._binding import (  # noqa: F401
-    CODE_BYTES, FORMATS, RULES, SsmqError, conv1d_update, dither_fill, library, requantize,
-    state_update,
+    CODE_BYTES, FORMATS, RULES, SsmqError, conv1d_update, dither_fill, library, replay,
+    requantize, state_update,
 )
 
-__all__ = ["state_update", "conv1d_update", "requantize", "dither_fill", "library", "SsmqError",
+__all__ = ["state_update", "conv1d_update", "requantize", "dither_fill", "replay", "library",
+           "SsmqError",
            "RULES",
            "FORMATS", "CODE_BYTES"]

@@ -46,7 +46,7 @@ class SsmqError(RuntimeError):
 
 
 EXPORTS = ("ssmq_state_update", "ssmq_state_update_ex", "ssmq_conv1d_update", "ssmq_requantize",
-           "ssmq_dither_fill", "ssmq_status_string", "ssmq_last_error")
+           "ssmq_dither_fill", "ssmq_replay", "ssmq_status_string", "ssmq_last_error")
 
 _lib = None
 
@@ -72,6 +72,9 @@ def library() -> ctypes.CDLL:
     L.ssmq_requantize.restype = _i32
     L.ssmq_dither_fill.argtypes = [_i32, _u32, _u32, _u32, _u64, _i64, _i32, _vp, _vp]
     L.ssmq_dither_fill.restype = _i32
+    L.ssmq_replay.argtypes = [ctypes.POINTER(QParams), _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
+                              _vp, _vp, _vp, _vp]
+    L.ssmq_replay.restype = _i32
     L.ssmq_status_string.argtypes = [_i32]
     L.ssmq_status_string.restype = ctypes.c_char_p
     L.ssmq_last_error.argtypes = []
@@ -174,3 +177,28 @@ def dither_fill(out, *, rule: str, seed=0, layer=0, step=0, entry_base=0, dither
     _check(library().ssmq_dither_fill(RULES[rule], int(seed) & 0xFFFFFFFF, int(layer) & 0xFFFFFFFF,
                                       int(step) & 0xFFFFFFFF, int(entry_base), out.numel(),
                                       int(dither_block), _ptr(out), _stream(stream, out)))
+
+
+def replay(h0, a, w, err, *, rule: str, fmt: str, ref=None, codes=None, scale=None, h_final=None,
+           block_steps=None, dither_block=16, scale_group=0, seed=0, layer=0, step=0,
+           entry_base=0, stream=None) -> None:
+    """ssmq_replay: open-loop replay of decays a and writes w [T, n] from h0 [n]; err
+    (and ref) [ceil(T / block_steps), n] float64 are written, and the final codes,
+    scales and reference state when given."""
+    n = h0.numel()
+    steps = a.shape[0] if a.dim() == 2 else (0 if a.numel() == 0 else a.numel() // max(n, 1))
+    if a.numel() != steps * n or w.numel() != steps * n:
+        raise ValueError("a and w must be [steps, n]")
+    bs = int(block_steps or max(steps, 1))
+    if err.dtype != torch.float64 or err.numel() != ((steps + bs - 1) // bs) * n:
+        raise ValueError("err must be float64 [ceil(steps / block_steps), n]")
+    if ref is not None and (ref.dtype != torch.float64 or ref.numel() != err.numel()):
+        raise ValueError("ref must be shaped as err")
+    if codes is not None and (codes.numel() * ENTRIES_PER_CODE[fmt] != n
+                              or codes.element_size() != CODE_BYTES[fmt]):
+        raise ValueError("codes must hold n entries of the format")
+    q = qparams(rule, fmt, dither_block=dither_block, scale_group=scale_group, seed=seed,
+                layer=layer, step=step, entry_base=entry_base)
+    _check(library().ssmq_replay(ctypes.byref(q), n, steps, bs, _ptr(h0), _ptr(a), _ptr(w),
+                                 _ptr(err), _ptr(ref), _ptr(codes), _ptr(scale), _ptr(h_final),
+                                 _stream(stream, h0)))

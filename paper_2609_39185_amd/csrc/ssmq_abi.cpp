@@ -64,15 +64,8 @@ ssmq::Thr make_thr(int rule, uint32_t seed, uint32_t layer, uint32_t step, int32
     else if (rule == SSMQ_SR) toff[k] = k * ssmq::kSrEntry;
     else toff[k] = 0u;
   }
-  if (rule == SSMQ_WEYL) {
-    th.key = ssmq::kWeylA + ssmq::kWeylB + ssmq::kWeylL * layer + ssmq::kWeylS * seed +
-             ssmq::kWeylPhi * step;
-  } else if (rule == SSMQ_SR) {
-    uint32_t k = ssmq::fmix32(seed);
-    k = ssmq::fmix32(k ^ (layer * ssmq::kSrLayer));
-    k = ssmq::fmix32(k ^ (step * ssmq::kSrStep));
-    th.key = k;
-  }
+  if (rule == SSMQ_WEYL) th.key = ssmq::weyl_step_key(seed, layer, step);
+  else if (rule == SSMQ_SR) th.key = ssmq::sr_step_key(ssmq::sr_seed_key(seed, layer), step);
   return th;
 }
 
@@ -330,6 +323,47 @@ ssmq_status ssmq_dither_fill(int32_t rule, uint32_t seed, uint32_t layer, uint32
   uint32_t unused[16];
   a.thr = make_thr(rule, seed, layer, step, dither_block, unused);
   hipError_t e = ssmq::launch_dither(a, rule, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+ssmq_status ssmq_replay(const ssmq_qparams* q, int64_t n, int32_t steps, int32_t block_steps,
+                        const float* h0, const float* a, const float* w, double* err, double* ref,
+                        void* codes, float* scale, float* h_final, void* stream) {
+  ssmq_status st = check_qparams(q);
+  if (st != SSMQ_OK) return st;
+  if (q->flags != 0) return fail(SSMQ_EINVAL, "the replay takes no flags");
+  if (n < 0 || n % 4 != 0) return fail(SSMQ_EINVAL, "n = %lld is not a multiple of 4 >= 0",
+                                       static_cast<long long>(n));
+  if (steps < 0) return fail(SSMQ_EINVAL, "steps < 0");
+  if (block_steps < 1) return fail(SSMQ_EINVAL, "block_steps < 1");
+  const bool scaled = is_scaled(q->format);
+  const int64_t group = q->scale_group;
+  if (scaled && !(is_pow2(group) && group >= 4 && group <= 256))
+    return fail(SSMQ_EUNSUPPORTED, "replay scale groups are powers of two from 4 to 256 entries");
+  if (scaled && n % group != 0)
+    return fail(SSMQ_EINVAL, "n must be a multiple of the scale group");
+  if (n == 0) return ok();
+  if (!h0 || (steps > 0 && (!a || !w || !err)))
+    return fail(SSMQ_EINVAL, "h0, a, w and err are required");
+  if (!aligned(h0, 16) || (a && !aligned(a, 16)) || (w && !aligned(w, 16)) ||
+      (err && !aligned(err, 16)) || (ref && !aligned(ref, 16)) || (codes && !aligned(codes, 16)) ||
+      (h_final && !aligned(h_final, 16)) || (scale && !aligned(scale, 4)))
+    return fail(SSMQ_EALIGN, "h0, a, w, err, ref, codes and h_final must be 16-byte aligned");
+  if ((n / 4 + 255) / 256 > 0x7FFFFFFFLL) return fail(SSMQ_EUNSUPPORTED, "n too large for one launch");
+  ssmq::ReplayArgs r{};
+  r.h0 = h0; r.a = a; r.w = w; r.err = err; r.ref = ref; r.codes = codes;
+  r.scale = scaled ? scale : nullptr; r.h_final = h_final;
+  r.n = n; r.steps = steps; r.block_steps = block_steps;
+  r.lanes_per_group = scaled ? static_cast<int32_t>(group / 4) : 1;
+  r.group_shift = scaled ? log2i(group) : 0;
+  r.entry_base = q->entry_base;
+  r.step0 = q->step;
+  uint32_t unused[16];
+  r.thr = make_thr(q->rule, q->seed, q->layer, q->step, q->dither_block, unused);
+  r.weyl_key0 = ssmq::weyl_step_key(q->seed, q->layer, q->step);
+  r.sr_key0 = ssmq::sr_seed_key(q->seed, q->layer);
+  hipError_t e = ssmq::launch_replay(r, q->format, q->rule, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SSMQ_EDEVICE, "kernel launch: %s", hipGetErrorString(e));
   return ok();
 }

@@ -71,6 +71,19 @@ __host__ __device__ inline uint32_t fmix32(uint32_t h) {
   return h;
 }
 
+// Per-step threshold keys (host and device). Weyl: the entry-independent part
+// A + B + L layer + S seed + Phi t of the accumulator; hash SR: the chained key
+// fmix32(fmix32(fmix32(seed) ^ layer * kSrLayer) ^ t * kSrStep).
+__host__ __device__ inline uint32_t weyl_step_key(uint32_t seed, uint32_t layer, uint32_t step) {
+  return kWeylA + kWeylB + kWeylL * layer + kWeylS * seed + kWeylPhi * step;
+}
+__host__ __device__ inline uint32_t sr_seed_key(uint32_t seed, uint32_t layer) {
+  return fmix32(fmix32(seed) ^ (layer * kSrLayer));
+}
+__host__ __device__ inline uint32_t sr_step_key(uint32_t seed_key, uint32_t step) {
+  return fmix32(seed_key ^ (step * kSrStep));
+}
+
 // A chunk is the unit one lane loads and stores: V entries in CB bytes (16, or
 // 8 for INT4). Scaled formats keep one fp32 scale per group of entries;
 // qmax is the value the group maximum is mapped to.
@@ -543,6 +556,17 @@ __device__ inline chunk_t<F> quantize_any(const float (&h)[Traits<F>::V], float 
   } else {
     return quantize_chunk<F, R>(h, tg, maybe_nan);
   }
+}
+
+// The exact fp32 value of one code (E4M3 and INT without the group scale).
+template <int F>
+__device__ inline float code_value(uint32_t c) {
+  if constexpr (F == kBF16) return __uint_as_float(c << 16);
+  else if constexpr (F == kFP16) return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(c)));
+  else if constexpr (F == kE4M3) return __builtin_amdgcn_cvt_f32_fp8(static_cast<int>(c), 0);
+  else if constexpr (F == kINT8) return static_cast<float>(static_cast<int32_t>(c << 24) >> 24);
+  else if constexpr (F == kINT4) return static_cast<float>(static_cast<int32_t>(c << 28) >> 28);
+  else return __uint_as_float(c);
 }
 
 // ---------------------------------------------------------------------------

@@ -12,6 +12,8 @@
 //   k_requant      fp32 -> codes for fp16 / bf16 / fp32, one chunk per thread.
 //   k_requant_scaled fp32 -> E4M3 / INT8 / INT4 codes with group scales.
 //   k_dither_fill  the 24-bit thresholds themselves.
+//   k_replay       open-loop replay of recorded decays and writes: a reference
+//                  and a stored trajectory per entry, iterated in registers.
 //
 // Layout. A chunk is 16 bytes of codes: V = 8 (fp16, bf16), 16 (E4M3) or 4
 // (fp32) consecutive entries of one state row. The LR = dstate / V chunks of a
@@ -431,6 +433,142 @@ __global__ __launch_bounds__(256) void k_dither_fill(DitherArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Open-loop replay. Thread q owns entries 4q .. 4q+3 for all steps: the fp32
+// reference h and the stored value hq stay in registers, so the only traffic is
+// the trace (a and w, 8 bytes per entry and step, nontemporal, the next step's
+// rows loaded while the current one is rounded) and the error sums per block.
+// Each step rounds fma(a, hq, w) with the exact software rounding of the
+// format (the per-entry functions of the fused kernels' exact path); the
+// scaled formats first reduce max|x| over the group's lanes. Lanes past n
+// (the grid's ragged end) run with zero inputs and store nothing, so the group
+// reductions always see whole groups.
+// ---------------------------------------------------------------------------
+template <int F, int R>
+__device__ inline void replay_round(const ReplayArgs& a, uint64_t e0, uint32_t step,
+                                    const float (&x)[4], float (&hq)[4], uint32_t (&code)[4],
+                                    float& scale) {
+  Thr th = a.thr;
+  th.step = step;
+  if constexpr (R == kWEYL) th.key = a.weyl_key0 + kWeylPhi * (step - a.step0);
+  else if constexpr (R == kSR) th.key = sr_step_key(a.sr_key0, step);
+  uint32_t thr[4];
+  if constexpr (R == kPHILOX) {
+    const ChunkThr<R, 4> t4 = chunk_thr<R, 4>(e0, th, 0u, nullptr);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) thr[k] = t4(k);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) thr[k] = entry_thr<R>(e0 + k, th);
+  }
+  if constexpr (Traits<F>::scaled) {
+    float m = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) m = fmaxf(m, __builtin_fabsf(x[k]));
+    const float s = group_scale<F>(__uint_as_float(lane_umax(__float_as_uint(m), a.lanes_per_group)));
+    const float r = recip_scale(s);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      code[k] = round_code<F, R>(x[k] * r, thr[k]);
+      hq[k] = code_value<F>(code[k]) * s;
+    }
+    scale = s;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      code[k] = round_code<F, R>(x[k], thr[k]);
+      hq[k] = code_value<F>(code[k]);
+    }
+  }
+}
+
+template <int F, int R>
+__global__ __launch_bounds__(256) void k_replay(ReplayArgs a) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t i0 = q * 4;
+  const bool live = i0 < a.n;
+  const uint64_t e0 = a.entry_base + static_cast<uint64_t>(i0);
+  float h[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (live) load_floats<4>(a.h0 + i0, h);
+  float hq[4];
+  uint32_t code[4];
+  float scale = 0.0f;
+  replay_round<F, R>(a, e0, a.step0, h, hq, code, scale);
+
+  double err[4] = {0.0, 0.0, 0.0, 0.0}, ref[4] = {0.0, 0.0, 0.0, 0.0};
+  float an[4] = {0.0f, 0.0f, 0.0f, 0.0f}, wn[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (live && a.steps > 0) {
+    const uint4 av = load_stream<uint4>(a.a + i0), wv = load_stream<uint4>(a.w + i0);
+    an[0] = __uint_as_float(av.x); an[1] = __uint_as_float(av.y);
+    an[2] = __uint_as_float(av.z); an[3] = __uint_as_float(av.w);
+    wn[0] = __uint_as_float(wv.x); wn[1] = __uint_as_float(wv.y);
+    wn[2] = __uint_as_float(wv.z); wn[3] = __uint_as_float(wv.w);
+  }
+  for (int32_t t = 1; t <= a.steps; ++t) {
+    float at[4], wt[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) { at[k] = an[k]; wt[k] = wn[k]; }
+    if (live && t < a.steps) {  // the next step's rows, in flight while this one rounds
+      const int64_t off = static_cast<int64_t>(t) * a.n + i0;
+      const uint4 av = load_stream<uint4>(a.a + off), wv = load_stream<uint4>(a.w + off);
+      an[0] = __uint_as_float(av.x); an[1] = __uint_as_float(av.y);
+      an[2] = __uint_as_float(av.z); an[3] = __uint_as_float(av.w);
+      wn[0] = __uint_as_float(wv.x); wn[1] = __uint_as_float(wv.y);
+      wn[2] = __uint_as_float(wv.z); wn[3] = __uint_as_float(wv.w);
+    }
+    float x[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      h[k] = fmaf(at[k], h[k], wt[k]);
+      x[k] = fmaf(at[k], hq[k], wt[k]);
+    }
+    replay_round<F, R>(a, e0, a.step0 + static_cast<uint32_t>(t), x, hq, code, scale);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const double d = static_cast<double>(hq[k]) - static_cast<double>(h[k]);
+      err[k] += d * d;
+      ref[k] += static_cast<double>(h[k]) * static_cast<double>(h[k]);
+    }
+    if (t % a.block_steps == 0 || t == a.steps) {
+      if (live) {
+        const int64_t off = static_cast<int64_t>((t - 1) / a.block_steps) * a.n + i0;
+        double2* pe = reinterpret_cast<double2*>(a.err + off);
+        pe[0] = make_double2(err[0], err[1]);
+        pe[1] = make_double2(err[2], err[3]);
+        if (a.ref) {
+          double2* pr = reinterpret_cast<double2*>(a.ref + off);
+          pr[0] = make_double2(ref[0], ref[1]);
+          pr[1] = make_double2(ref[2], ref[3]);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) { err[k] = 0.0; ref[k] = 0.0; }
+    }
+  }
+  if (!live) return;
+  if (a.codes) {
+    if constexpr (F == kFP32) {
+      *reinterpret_cast<uint4*>(static_cast<uint32_t*>(a.codes) + i0) =
+          make_uint4(code[0], code[1], code[2], code[3]);
+    } else if constexpr (F == kBF16 || F == kFP16) {
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.codes) + i0) =
+          make_uint2(code[0] | (code[1] << 16), code[2] | (code[3] << 16));
+    } else if constexpr (F == kINT4) {
+      static_cast<uint16_t*>(a.codes)[i0 / 4] =
+          static_cast<uint16_t>(code[0] | (code[1] << 4) | (code[2] << 8) | (code[3] << 12));
+    } else {
+      static_cast<uint32_t*>(a.codes)[i0 / 4] =
+          code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+    }
+  }
+  if constexpr (Traits<F>::scaled) {
+    if (a.scale && (threadIdx.x & (a.lanes_per_group - 1)) == 0)
+      a.scale[static_cast<int64_t>(e0 - a.entry_base) >> a.group_shift] = scale;
+  }
+  if (a.h_final)
+    *reinterpret_cast<float4*>(a.h_final + i0) = make_float4(h[0], h[1], h[2], h[3]);
+}
+
+// ---------------------------------------------------------------------------
 // Causal depthwise conv1d decode update: thread i = b * channels + c shifts its
 // channel's window by one, appends x[i] and writes
 // out[i] = (silu)(bias[c] + sum_k window[k] * weight[c][k]).
@@ -575,6 +713,29 @@ hipError_t launch_dither(const DitherArgs& a, int rule, hipStream_t s) {
     default: hipLaunchKernelGGL((k_dither_fill<kWEYL>), dim3(grid), dim3(256), 0, s, a); break;
   }
   return hipGetLastError();
+}
+
+template <int F>
+static hipError_t launch_replay_f(const ReplayArgs& a, int rule, hipStream_t s) {
+  const unsigned grid = static_cast<unsigned>((a.n / 4 + 255) / 256);
+  switch (rule) {
+    case kRTN: hipLaunchKernelGGL((k_replay<F, kRTN>), dim3(grid), dim3(256), 0, s, a); break;
+    case kSR: hipLaunchKernelGGL((k_replay<F, kSR>), dim3(grid), dim3(256), 0, s, a); break;
+    case kPHILOX: hipLaunchKernelGGL((k_replay<F, kPHILOX>), dim3(grid), dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((k_replay<F, kWEYL>), dim3(grid), dim3(256), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_replay(const ReplayArgs& a, int format, int rule, hipStream_t s) {
+  switch (format) {
+    case kFP16: return launch_replay_f<kFP16>(a, rule, s);
+    case kBF16: return launch_replay_f<kBF16>(a, rule, s);
+    case kE4M3: return launch_replay_f<kE4M3>(a, rule, s);
+    case kINT8: return launch_replay_f<kINT8>(a, rule, s);
+    case kINT4: return launch_replay_f<kINT4>(a, rule, s);
+    default: return launch_replay_f<kFP32>(a, rule, s);
+  }
 }
 
 hipError_t launch_conv1d(const ConvArgs& a, hipStream_t s) {

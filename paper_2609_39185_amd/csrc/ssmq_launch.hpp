@@ -111,6 +111,28 @@ struct DitherArgs {
   Thr thr;
 };
 
+// Open-loop replay of recorded decays and writes: four entries per thread.
+struct ReplayArgs {
+  const float* h0;          // [n]
+  const float* a;           // [steps][n]
+  const float* w;           // [steps][n]
+  double* err;              // [n_blocks][n]
+  double* ref;              // [n_blocks][n] or null
+  void* codes;              // final codes or null
+  float* scale;             // final group scales or null
+  float* h_final;           // final reference state or null
+  int64_t n;                // entries, a multiple of 4
+  int32_t steps, block_steps;
+  int32_t lanes_per_group;  // scaled formats: group / 4, a power of two <= 64
+  int32_t group_shift;      // log2(group)
+  uint64_t entry_base;      // a multiple of 4
+  uint32_t step0;           // step of the write of h0
+  uint32_t weyl_key0;       // Weyl key at step0
+  uint32_t sr_key0;         // hash SR seed-and-layer key
+  Thr thr;                  // lb, seed, layer (key and step set per step)
+};
+
+hipError_t launch_replay(const ReplayArgs& a, int format, int rule, hipStream_t s);
 hipError_t launch_update(const UpdateArgs& a, int format, int rule, int cfg, bool a_per_state,
                          hipStream_t s);
 hipError_t launch_requant(const RequantArgs& a, int format, int rule, hipStream_t s);

@@ -127,3 +127,32 @@ def test_dither_fill_validation(lib):
     assert L.ssmq_dither_fill(2, 0, 0, 0, 0, 16, 16, None, None) == EINVAL
     assert L.ssmq_dither_fill(2, 0, 0, 0, 0, 16, 16, FAKE + 2, None) == EALIGN
     assert L.ssmq_dither_fill(2, 0, 0, 0, 0, 0, 16, None, None) == 0
+
+
+def test_replay_validation(lib):
+    L = lib.library()
+    Q = lib.qparams
+
+    def rp(q, n=64, steps=8, bs=4, h0=FAKE, a=FAKE, w=FAKE, err=FAKE, ref=None, codes=None,
+           scale=None, hf=None):
+        return L.ssmq_replay(ctypes.byref(q) if q is not None else None, n, steps, bs, h0, a, w,
+                             err, ref, codes, scale, hf, None)
+
+    assert rp(None) == EINVAL
+    assert rp(Q("weyl", "bf16"), n=-4) == EINVAL
+    assert rp(Q("weyl", "bf16"), n=6) == EINVAL                    # not a multiple of 4
+    assert rp(Q("weyl", "bf16"), steps=-1) == EINVAL
+    assert rp(Q("weyl", "bf16"), bs=0) == EINVAL
+    assert rp(Q("weyl", "bf16", flags=1)) == EINVAL                # no checkpoint flag here
+    assert rp(Q("weyl", "bf16", entry_base=8)) == EINVAL           # a multiple of 16
+    assert rp(Q("weyl", "int8", scale_group=0)) == EUNSUPPORTED    # no per-head groups
+    assert rp(Q("weyl", "int8", scale_group=512)) == EUNSUPPORTED
+    assert rp(Q("weyl", "e4m3", scale_group=24)) == EUNSUPPORTED
+    assert rp(Q("weyl", "int4", scale_group=16), n=40) == EINVAL   # n not a multiple of the group
+    assert rp(Q("weyl", "bf16"), a=None) == EINVAL
+    assert rp(Q("weyl", "bf16"), err=None) == EINVAL
+    assert rp(Q("weyl", "bf16"), h0=FAKE + 4) == EALIGN
+    assert rp(Q("weyl", "bf16"), ref=FAKE + 8) == EALIGN
+    # empty traces never reach the device
+    assert rp(Q("weyl", "bf16"), n=0, h0=None, a=None, w=None, err=None) == 0
+    assert L.ssmq_last_error() == b""
