@@ -69,6 +69,9 @@ def parse_args():
     ap.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                     help="turn rocprofv3 CSV output (kernel trace with --stats, then --pmc "
                          "FETCH_SIZE, then --pmc WRITE_SIZE) into the summaries under profiles/")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_DIR", "NAME"),
+                    help="turn a rocprofv3 --kernel-trace --stats run of --replay into "
+                         "profiles/NAME.kernel_trace.md")
     ap.add_argument("--summarize-valu", metavar="PMC_DIR",
                     help="turn a rocprofv3 --pmc run of SQ_WAVES, SQ_INSTS_VALU, "
                          "SQ_ACTIVE_INST_VALU and GRBM_GUI_ACTIVE into profiles/...valu.md")
@@ -99,6 +102,8 @@ def main() -> int:
         return summarize_profiles(args.workload, *args.summarize_profiles)
     if args.summarize_valu:
         return summarize_valu(args.workload, args.summarize_valu)
+    if args.summarize_trace:
+        return summarize_replay_trace(*args.summarize_trace)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build measures one GPU only; the state update shards "
@@ -373,6 +378,12 @@ def replay_study(w, *, steps: int, batch: int, block: int, memory: str, device, 
     share = torch.bincount(bins.flatten(), minlength=n_bins).double() / bins.numel()
     nb = (steps + block - 1) // block
     stream = torch.cuda.current_stream(device)
+    # one small untimed replay per format loads the kernels before the timed launches
+    for fmt, g in formats:
+        tiny = torch.empty((1, 256), dtype=torch.float64, device=device)
+        ssmq.replay(h0[:256], a_tr[:1, :256].contiguous(), w_tr[:1, :256].contiguous(), tiny,
+                    rule="rtn", fmt=fmt, scale_group=g, stream=stream)
+    torch.cuda.synchronize()
     out, timing = {}, {}
     den_bins = None
     for fmt, g in formats:
@@ -752,6 +763,44 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
     return 0
 
 
+def summarize_replay_trace(trace_dir: str, name: str) -> int:
+    """Write profiles/<name>.kernel_trace.md from a kernel trace of the replay study
+    (PROFILE_COMMANDS["replay_trace"]): per k_replay instance, calls and durations,
+    and the trace rate 8 B x entries x steps / average duration."""
+    import re
+
+    stats = _csv_rows(trace_dir, "kernel_stats.csv")
+    m = re.search(r"--steps (\d+)", PROFILE_COMMANDS["replay_trace"])
+    steps = int(m.group(1))
+    from paper_2609_39185_amd import workloads as wl
+    w = wl.WORKLOADS["m1_long"]
+    n = w.batch * w.nheads * w.dstate
+    fmts = {v: k for k, v in _FMT_CODE.items()}
+    rules = {v: k for k, v in _RULE_CODE.items()}
+    lines = [f"# Kernel trace of the replay study ({n} entries x {steps} steps per launch)", "",
+             "Command (repository root as $R, run from /tmp with TMPDIR=/tmp):", "",
+             f"    {PROFILE_COMMANDS['replay_trace']}",
+             f"    {PROFILE_COMMANDS['replay_trace_summary']}", "",
+             "The longest call of each instance is a full-size launch: the RTN instances also run "
+             "one untimed 256-entry, one-step launch, the hash-SR instances run twice at full size "
+             "(seeds 0 and 1). Trace rate = 8 B x entries x steps / the full-size duration.", "",
+             "| kernel | format:rule | calls | full-size launch us | trace GB/s |",
+             "|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: r["Name"]):
+        km = re.search(r"k_replay<(\d+), (\d+)>", r["Name"])
+        if not km:
+            continue
+        key = f"{fmts[int(km.group(1))]}:{rules[int(km.group(2))]}"
+        mx = float(r["MaxNs"]) / 1e3
+        lines.append(f"| `{_short_kernel(r['Name'])}` | {key} | {r['Calls']} | {mx:.1f} | "
+                     f"{8 * n * steps / (mx * 1e3):.0f} |")
+    os.makedirs(PROFILE_DIR, exist_ok=True)
+    with open(os.path.join(PROFILE_DIR, f"{name}.kernel_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 def summarize_valu(workload: str, pmc_dir: str) -> int:
     """Write profiles/k_update_slab.<workload>.valu.md: per variant, VALU
     instructions per wave and per entry (lane operations), and the VALU busy
@@ -806,6 +855,10 @@ PROFILE_COMMANDS = {
             "-d $R/gpurun_out/pmc_busy -o run -- python3 $R/bench.py --steps 2 --warmup 0 "
             "--layers 4 --cpu-seconds 0 --no-ceiling",
     "valu_summary": "python3 $R/bench.py --summarize-valu $R/gpurun_out/pmc_busy",
+    "replay_trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof_replay "
+                    "-o run -- python3 $R/bench.py --replay --steps 4096",
+    "replay_trace_summary": "python3 $R/bench.py --summarize-trace $R/gpurun_out/prof_replay "
+                            "k_replay.m1_long",
 }
 
 

@@ -65,3 +65,19 @@ def test_profile_summary_scales_counters_by_the_calibration_kernel(tmp_path, mon
     rec["kernel_sources_sha256"] = "0" * 64
     json.dump(rec, open(tmp_path / "profiles" / "k_update_slab.hybrid_m2_stack.traffic.json", "w"))
     assert bench.load_traffic("hybrid_m2_stack") is None
+
+
+def test_replay_trace_summary_rates(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "PROFILE_DIR", str(tmp_path / "profiles"))
+    name = "void ssmq::k_replay<4, 2>(ssmq::ReplayArgs)"
+    _write_csv(str(tmp_path / "trace" / "run_kernel_stats.csv"),
+               [{"Name": name, "Calls": 1, "TotalDurationNs": 10_000_000, "AverageNs": 10_000_000,
+                 "MinNs": 10_000_000, "MaxNs": 10_000_000},
+                {"Name": "void other_kernel()", "Calls": 5, "TotalDurationNs": 5, "AverageNs": 1,
+                 "MinNs": 1, "MaxNs": 1}])
+    assert bench.summarize_replay_trace(str(tmp_path / "trace"), "k_replay.test") == 0
+    text = open(tmp_path / "profiles" / "k_replay.test.kernel_trace.md").read()
+    row = [ln for ln in text.splitlines() if "k_replay<4, 2>" in ln][0]
+    # 8 B x 1,310,720 entries x 4096 steps in 10 ms
+    assert "int8:weyl" in row and row.rstrip(" |").endswith(f"{8 * 1310720 * 4096 / 1e7:.0f}")
+    assert "other_kernel" not in text
