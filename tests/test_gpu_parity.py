@@ -428,3 +428,54 @@ def test_e4m3_head_scale_overshoot_saturates(ssmq, rule, over):
     assert r_codes.ravel()[entry] == 0x7E and np.count_nonzero(r_codes) == 1
     assert np.array_equal(got, r_codes), (got.ravel()[entry], r_codes.ravel()[entry])
     assert np.array_equal(sc.cpu().numpy(), r_scale)
+
+
+@pytest.mark.parametrize("fmt,rule,batch", [("bf16", "weyl", 2304), ("e4m3", "sr", 4608)])
+def test_state_beyond_4gib(ssmq, fmt, rule, batch):
+    """One call on a state past 2^31 entries and 4 GiB of codes (64-bit byte offsets
+    and flat indices): hybrid-shaped heads at a large batch, sampled tiles up to the
+    last one against the oracle."""
+    import paper_2609_39185_amd as m
+    H, P, N, G = 128, 64, 128, 8
+    n = batch * H * P * N
+    assert n > 2 ** 31 and n * ssmq.CODE_BYTES[fmt] > 2 ** 32
+    say(f"case large state {fmt} {rule}: batch {batch}, {n} entries")
+    A, D = wl.layer_params("mamba2", H, N, 600, device=DEV)
+    x, dt, B, C = wl.step_inputs(batch, H, P, N, G, 601, device=DEV)
+    codes = torch.empty((batch, H, P, N), dtype=wl.CODE_TORCH_DTYPE[fmt], device=DEV)
+    scale = torch.empty(batch * H, device=DEV) if fmt == "e4m3" else None
+    for b0 in range(0, batch, 256):  # fill in slices to bound the temporaries
+        c, s = wl.initial_state(fmt, min(256, batch - b0), H, P, N, 602 + b0, device=DEV)
+        codes[b0:b0 + c.shape[0]].copy_(c)
+        if scale is not None:
+            scale[b0 * H:(b0 + c.shape[0]) * H].copy_(s)
+        del c, s
+    tiles = [0, 12345, batch * H // 2 + 7, batch * H - 2, batch * H - 1]
+    before = {t: codes.view(-1, P, N)[t].cpu().clone() for t in tiles}
+    sbefore = None if scale is None else scale.cpu().clone()
+    y = torch.empty((batch, H, P), device=DEV)
+    m.state_update(codes, scale, x, dt, A, B, C, D, y, rule=rule, fmt=fmt, dither_block=128,
+                   step=31, layer=4)
+    torch.cuda.synchronize()
+    from ._parity import code_stats
+    hpg = H // G
+    for t in tiles:
+        bb, hh = divmod(t, H)
+        gg = hh // hpg
+        cs = lambda v: v.detach().cpu()
+        r_codes, r_scale, r_y, r_h = oracle.state_update(
+            fmt, rule, wl.to_numpy_codes(fmt, before[t].view(1, 1, P, N)),
+            None if sbefore is None else sbefore[t:t + 1].numpy(),
+            cs(x[bb:bb + 1, hh:hh + 1]).numpy(), cs(dt[bb:bb + 1, hh:hh + 1]).numpy(),
+            cs(A[hh:hh + 1]).numpy(), cs(B[bb:bb + 1, gg:gg + 1]).numpy(),
+            cs(C[bb:bb + 1, gg:gg + 1]).numpy(), cs(D[hh:hh + 1]).numpy(),
+            step=31, layer=4, block=128, entry_base=t * P * N)
+        got = wl.to_numpy_codes(fmt, cs(codes.view(-1, P, N)[t]).view(1, 1, P, N))
+        nd, ulp = code_stats(fmt, got, r_codes)
+        assert nd <= 1 and ulp <= 1, (t, nd, ulp)
+        if scale is not None:
+            assert np.array_equal(cs(scale[t:t + 1]).numpy(), r_scale), t
+        Ch = cs(C[bb, gg]).numpy().astype(np.float64)
+        mag = np.abs(Ch[None, :] * r_h[0, 0]).sum(-1) + abs(float(D[hh]) * cs(x[bb, hh]).numpy())
+        yg = cs(y[bb, hh]).numpy().astype(np.float64)
+        assert np.all(np.abs(yg - r_y[0, 0]) <= 1e-5 * (mag + np.abs(r_y[0, 0]))), t
