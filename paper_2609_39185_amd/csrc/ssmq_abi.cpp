@@ -217,6 +217,8 @@ ssmq_status ssmq_state_update_ex(const ssmq_dims* dims, const ssmq_qparams* q,
         head_chunks / (ssmq::kSlabThreads[cfg] * ssmq::kSlabChunks[cfg]));
     a.lanes_per_group = scaled ? static_cast<int32_t>(group / 16) : 1;
   }
+  if (cfg >= 0)
+    a.n128 = (d.dstate == 128 && (!scaled || a.lanes_per_group == 0 || a.lanes_per_group == 8)) ? 1 : 0;
   if (cfg >= 0) {  // threshold base advance per pass of NT chunks
     const int64_t step_entries = static_cast<int64_t>(ssmq::kSlabThreads[cfg]) * V;
     a.pass_thr_ok = 1;

@@ -78,6 +78,7 @@ struct UpdateArgs {
   uint32_t toff[16];        // threshold offset of entry k of a chunk
   uint32_t pass_thr_inc;    // slab kernels: threshold base increment per pass ...
   int32_t pass_thr_ok;      // ... when a pass advances by whole dither blocks (or SR)
+  int32_t n128;             // slab kernels: dstate 128, groups of 128 entries or one head
   FastDiv div_headdim, div_nheads, div_hpg, div_slabs;  // index arithmetic
 };
 
