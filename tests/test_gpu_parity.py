@@ -479,3 +479,83 @@ def test_state_beyond_4gib(ssmq, fmt, rule, batch):
         mag = np.abs(Ch[None, :] * r_h[0, 0]).sum(-1) + abs(float(D[hh]) * cs(x[bb, hh]).numpy())
         yg = cs(y[bb, hh]).numpy().astype(np.float64)
         assert np.all(np.abs(yg - r_y[0, 0]) <= 1e-5 * (mag + np.abs(r_y[0, 0]))), t
+
+
+@pytest.mark.parametrize("fmt,rule,group", [("bf16", "weyl", 0), ("int8", "sr", 128),
+                                            ("e4m3", "philox", 0)])
+def test_step_counter_wraps_and_resume_is_exact(ssmq, fmt, rule, group):
+    """Steps 2^32 - 2, 2^32 - 1, 0, 1 (the counter is taken mod 2^32) match the
+    oracle step by step, and saving the state to the host after two steps and
+    restoring it resumes bit for bit: the codes (and scales) plus the step counter
+    are the whole state."""
+    import paper_2609_39185_amd as m
+    b, H, P, N, G = 2, 4, 64, 128, 2
+    A, D = wl.layer_params("mamba2", H, N, 70)
+    codes, scale = wl.initial_state(fmt, b, H, P, N, 71, group=group)
+    steps = [2 ** 32 - 2, 2 ** 32 - 1, 0, 1]
+    inputs = [wl.step_inputs(b, H, P, N, G, 72 + k) for k in range(4)]
+
+    def run(st, sc, ks):
+        for k in ks:
+            x, dt, B, C = (v.to(DEV) for v in inputs[k])
+            y = torch.empty((b, H, P), device=DEV)
+            m.state_update(st, sc, x, dt, A.to(DEV), B, C, D.to(DEV), y, rule=rule, fmt=fmt,
+                           dither_block=128, scale_group=group, step=steps[k], layer=6)
+        torch.cuda.synchronize()
+
+    st = codes.to(DEV)
+    sc = None if scale is None else scale.to(DEV)
+    ref_c, ref_s = wl.to_numpy_codes(fmt, codes), None if scale is None else scale.numpy()
+    from ._parity import code_stats
+    for k in range(4):
+        run(st, sc, [k])
+        x, dt, B, C = (v.numpy() for v in inputs[k])
+        want = oracle.state_update(fmt, rule, ref_c, ref_s, x, dt, A.numpy(), B, C, D.numpy(),
+                                   step=steps[k], layer=6, block=128, group=group)
+        got = wl.to_numpy_codes(fmt, st)
+        nd, ulp = code_stats(fmt, got, want[0])
+        assert nd <= 1e-4 * got.size and ulp <= 1, (k, nd, ulp)
+        ref_c, ref_s = got, None if sc is None else sc.cpu().numpy()  # teacher-forced
+    # resume: two steps, a round trip through host memory, two more == four straight
+    st2 = codes.to(DEV)
+    sc2 = None if scale is None else scale.to(DEV)
+    run(st2, sc2, [0, 1])
+    saved = (st2.cpu(), None if sc2 is None else sc2.cpu())
+    st3 = saved[0].to(DEV)
+    sc3 = None if saved[1] is None else saved[1].to(DEV)
+    run(st3, sc3, [2, 3])
+    assert torch.equal(st3.cpu(), st.cpu())
+    if sc is not None:
+        assert torch.equal(sc3.cpu(), sc.cpu())
+
+
+def test_full_size_m1_long_layer(ssmq):
+    """One layer of the long-horizon Mamba-1 workload (batch 16, d_inner 5120, N 16,
+    fp16, dither block 16) in the row kernel the study uses: sampled channels of
+    every sequence against the oracle."""
+    import paper_2609_39185_amd as m
+    w = wl.WORKLOADS["m1_long"]
+    b, d, N = w.batch, w.nheads, w.dstate
+    A, D = wl.layer_params("mamba1", d, N, 800, device=DEV)
+    x, dt, B, C = wl.step_inputs(b, d, 1, N, 1, 801, device=DEV)
+    codes, _ = wl.initial_state("fp16", b, d, 1, N, 802, device=DEV)
+    before = codes.cpu().clone()
+    y = torch.empty((b, d, 1), device=DEV)
+    say(f"case full size m1_long layer: {b * d * N} entries")
+    for rule in ("weyl", "sr"):
+        st = codes.clone()
+        m.state_update(st, None, x, dt, A, B, C, D, y, rule=rule, fmt="fp16", dither_block=16,
+                       step=1234, layer=17)
+        torch.cuda.synchronize()
+        chans = np.array([0, 1, 777, 2560, d - 1])
+        for bb in (0, b - 1):
+            sl = slice(int(chans.min()), int(chans.max()) + 1)
+            cs = lambda v: v.detach().cpu()
+            r_codes, _, r_y, _ = oracle.state_update(
+                "fp16", rule, wl.to_numpy_codes("fp16", before[bb:bb + 1, sl]), None,
+                cs(x[bb:bb + 1, sl]).numpy(), cs(dt[bb:bb + 1, sl]).numpy(), cs(A[sl]).numpy(),
+                cs(B[bb:bb + 1]).numpy(), cs(C[bb:bb + 1]).numpy(), cs(D[sl]).numpy(),
+                step=1234, layer=17, block=16, entry_base=(bb * d + sl.start) * N)
+            got = wl.to_numpy_codes("fp16", cs(st[bb:bb + 1, sl]))
+            nd = int(np.count_nonzero(got != r_codes))
+            assert nd <= max(1, 1e-4 * got.size), (rule, bb, nd)
