@@ -390,16 +390,10 @@ __device__ inline bool chunk_has_nan(const float (&v)[V]) {
   return n;
 }
 
-// E4M3 values can exceed 448 only by the scale's own rounding (the scale maps
-// the group maximum to 448): the stochastic conversions, which do not saturate,
-// get values clamped with v_med3_f32 (clamping first is eq. (dither) on the
-// saturated grid); round-to-nearest needs no clamp below 464, which a scaled
-// value never reaches. clamp = false (wave-uniform): the caller knows that no
-// value of the group exceeds 448 (fl32(max|h| r) <= 448; rounding is monotonic).
 template <int F, int R, typename TG>
 __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG& tg,
-                                       bool maybe_nan, bool clamp = true) {
-  constexpr int V = Traits<F>::V;
+                                       bool maybe_nan) {
+  static_assert(F == kBF16 || F == kFP16 || F == kFP32, "unscaled float formats");
   uint32_t w[4];
   if constexpr (F == kFP32) {
 #pragma unroll
@@ -422,7 +416,7 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG&
       }
       w[i] = __builtin_bit_cast(uint32_t, p);
     }
-  } else if constexpr (F == kFP16) {
+  } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       v2h p;
@@ -436,35 +430,71 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG&
       }
       w[i] = __builtin_bit_cast(uint32_t, p);
     }
-  } else {  // E4M3, values already scaled
-    float q[V];
+  }
+  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, Traits<F>::V>(v, maybe_nan)) != 0) {
 #pragma unroll
-    for (int k = 0; k < V; ++k) q[k] = v[k];
-    if (R != kRTN && clamp) {
-#pragma unroll
-      for (int k = 0; k < V; ++k) q[k] = __builtin_amdgcn_fmed3f(v[k], -448.0f, 448.0f);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k = 4 * i;
-      int d;  // all four bytes are written: the previous contents are don't-care
-      if constexpr (R == kRTN) {
-        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k], q[k + 1], static_cast<int>(__float_as_uint(q[k])), false);
-        d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k + 2], q[k + 3], d, true);
-      } else {
-        const uint32_t t0 = signed_thr(tg(k), q[k]);  // dies here
-        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k], t0, static_cast<int>(t0), 0);
-        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 1], signed_thr(tg(k + 1), q[k + 1]), d, 1);
-        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 2], signed_thr(tg(k + 2), q[k + 2]), d, 2);
-        d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 3], signed_thr(tg(k + 3), q[k + 3]), d, 3);
-      }
-      w[i] = static_cast<uint32_t>(d);
+    for (int k = 0; k < Traits<F>::V; ++k) {
+      if (needs_exact_path<F, R>(v[k])) patch_code<F>(w, k, round_code<F, R>(v[k], tg(k)));
     }
   }
-  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, V>(v, maybe_nan)) != 0) {
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// E4M3 chunk of 16 entries: h the fp32 values, r = fl32(1 / s) of their group.
+// Values q = fl32(h r) exceed 448 only by the scale's own rounding (the scale
+// maps the group maximum to 448): the stochastic conversions, which do not
+// saturate, get q clamped with v_med3_f32 (clamping first is eq. (dither) on
+// the saturated grid) unless the caller knows that no q of the group passes 448
+// (clamp = false, wave-uniform: fl32(max|h| r) <= 448, rounding is monotonic);
+// round-to-nearest needs no clamp below 464, which a scaled value never
+// reaches. The exact path takes NaN (maybe_nan: a NaN may be among h) and
+// |q| < 2^-10; since fl32(x r) is monotonic in x, the smallest |q| is
+// fl32(min|h| r), one product per chunk.
+template <int R, typename TG>
+__device__ inline uint4 quantize_e4m3_chunk(const float (&h)[16], float r, const TG& tg,
+                                            bool maybe_nan, bool clamp) {
+  float q[16];
 #pragma unroll
-    for (int k = 0; k < V; ++k) {
-      if (needs_exact_path<F, R>(v[k])) patch_code<F>(w, k, round_code<F, R>(v[k], tg(k)));
+  for (int k = 0; k < 16; ++k) q[k] = h[k] * r;
+  // Philox SR always clamps: its generator already fills the registers that a
+  // second code path would need.
+  if (R != kRTN && (R == kPHILOX || clamp)) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) q[k] = __builtin_amdgcn_fmed3f(q[k], -448.0f, 448.0f);
+  }
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int k = 4 * i;
+    int d;  // all four bytes are written: the previous contents are don't-care
+    if constexpr (R == kRTN) {
+      d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k], q[k + 1], static_cast<int>(__float_as_uint(q[k])), false);
+      d = __builtin_amdgcn_cvt_pk_fp8_f32(q[k + 2], q[k + 3], d, true);
+    } else {
+      const uint32_t t0 = signed_thr(tg(k), q[k]);  // dies here
+      d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k], t0, static_cast<int>(t0), 0);
+      d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 1], signed_thr(tg(k + 1), q[k + 1]), d, 1);
+      d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 2], signed_thr(tg(k + 2), q[k + 2]), d, 2);
+      d = __builtin_amdgcn_cvt_sr_fp8_f32(q[k + 3], signed_thr(tg(k + 3), q[k + 3]), d, 3);
+    }
+    w[i] = static_cast<uint32_t>(d);
+  }
+  bool rare = maybe_nan;
+  if constexpr (R != kRTN) {
+    float mn = __builtin_fabsf(h[0]);
+#pragma unroll
+    for (int k = 1; k < 16; ++k) mn = fminf(mn, __builtin_fabsf(h[k]));
+    rare = rare || !(mn * r >= 0x1p-10f);
+  }
+  if (__builtin_amdgcn_ballot_w64(rare) != 0) {
+    // The products are formed again here (r passed through an empty asm so that
+    // they are not shared with q): q then needs no copy to survive the clamp.
+    float rr = r;
+    asm volatile("" : "+v"(rr));
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float v = h[k] * rr;
+      if (needs_exact_path<kE4M3, R>(v)) patch_code<kE4M3>(w, k, round_code<kE4M3, R>(v, tg(k)));
     }
   }
   return make_uint4(w[0], w[1], w[2], w[3]);
@@ -549,10 +579,7 @@ __device__ inline chunk_t<F> quantize_any(const float (&h)[Traits<F>::V], float 
   if constexpr (is_int_fmt<F>) {
     return quantize_int_chunk<F, R>(h, r, r * 0x1p24f, tg, maybe_nan);
   } else if constexpr (F == kE4M3) {
-    float v[16];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = h[k] * r;
-    return quantize_chunk<F, R>(v, tg, maybe_nan, clamp);
+    return quantize_e4m3_chunk<R>(h, r, tg, maybe_nan, clamp);
   } else {
     return quantize_chunk<F, R>(h, tg, maybe_nan);
   }
