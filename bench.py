@@ -64,6 +64,8 @@ def parse_args():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the timed steps from one HIP graph (removes host launch gaps)")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the streaming-kernel bandwidth ceiling")
     ap.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
@@ -151,7 +153,7 @@ def main() -> int:
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream(dev)
 
-    def one_step(fmt, rule, t, events=None):
+    def one_step(fmt, rule, t, events=None, on=None):
         for ell, lay in enumerate(layers):
             st, sc = lay["states"][fmt]
             if events is not None:
@@ -159,7 +161,7 @@ def main() -> int:
             ssmq.state_update(st, sc, lay["x"], lay["dt"], lay["A"], lay["B"], lay["C"], lay["D"],
                               lay["y"], rule=rule, fmt=fmt, dither_block=w.dither_block,
                               scale_group=wl.scale_group_of(w, fmt), layer=ell, step=t, seed=0,
-                              stream=stream)
+                              stream=on or stream)
             if events is not None:
                 events[ell][1].record(stream)
 
@@ -176,11 +178,25 @@ def main() -> int:
         # their number is the average launch duration (gaps included).
         start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        start.record(stream)
-        for k in range(args.steps):
-            one_step(fmt, rule, t_global)
-            t_global += 1
-        stop.record(stream)
+        if args.graph:
+            # All launches of the timed steps (each with its own step t) are captured
+            # into one HIP graph beforehand; the timed region replays it once.
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                cap = torch.cuda.current_stream(dev)
+                for k in range(args.steps):
+                    one_step(fmt, rule, t_global + k, on=cap)
+            torch.cuda.synchronize()
+            start.record(stream)
+            graph.replay()
+            stop.record(stream)
+            t_global += args.steps
+        else:
+            start.record(stream)
+            for k in range(args.steps):
+                one_step(fmt, rule, t_global)
+                t_global += 1
+            stop.record(stream)
         torch.cuda.synchronize()
         total_ms = start.elapsed_time(stop)
         ms_step = total_ms / args.steps
@@ -269,7 +285,8 @@ def main() -> int:
                    "headdim": P, "dstate": N, "ngroups": G, "format": head_fmt,
                    "rule": head_rule, "dither_block": w.dither_block,
                    "scale_group": (wl.scale_group_of(w, head_fmt) or P * N)
-                   if head_fmt in ("e4m3", "int8", "int4") else None},
+                   if head_fmt in ("e4m3", "int8", "int4") else None,
+                   "launch": "hip_graph" if args.graph else "stream"},
         "pct_of_peak": head["pct_of_peak"],
         "steps_per_s": head["steps_per_s"],
         "roofline": roof,
