@@ -108,7 +108,7 @@ def main() -> int:
         return summarize_replay_trace(*args.summarize_trace)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build measures one GPU only; the state update shards "
+        print(json.dumps({"error": "this benchmark measures one GPU only; the state update shards "
                                    "by batch or head with no communication, so --gpus must be 1"}))
         return 2
 
@@ -750,8 +750,8 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
         f.write("\n")
 
     lines = [f"# k_update_slab on {workload}: HBM traffic per launch", "",
-             "Commands (repository root as $R, run from /tmp with TMPDIR=/tmp):", ""]
-    lines += [f"    {c}" for c in PROFILE_COMMANDS.values()]
+             "Commands (repository root as $R, an output directory as $OUT, run from /tmp with TMPDIR=/tmp):", ""]
+    lines += [f"    {PROFILE_COMMANDS[k]}" for k in ("trace", "fetch", "write", "summary")]
     lines += ["", f"Calibration: torch.neg over {CAL_BYTES} B in and out reads "
                   f"FETCH_SIZE x {f_fetch:.4f}, WRITE_SIZE x {f_write:.4f} of the true bytes.", "",
               "| variant | kernel | FETCH KiB | WRITE KiB | traffic B | algorithmic B | ratio |",
@@ -764,7 +764,7 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
         f.write("\n".join(lines) + "\n")
 
     lines = [f"# Kernel trace of the default bench run on {workload}", "",
-             "Command (repository root as $R, run from /tmp with TMPDIR=/tmp):", "",
+             "Command (repository root as $R, an output directory as $OUT, run from /tmp with TMPDIR=/tmp):", "",
              f"    {PROFILE_COMMANDS['trace']}", "",
              "| kernel | calls | avg us | min us | max us | total ms |", "|---|---|---|---|---|---|"]
     for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:16]:
@@ -795,7 +795,7 @@ def summarize_replay_trace(trace_dir: str, name: str) -> int:
     fmts = {v: k for k, v in _FMT_CODE.items()}
     rules = {v: k for k, v in _RULE_CODE.items()}
     lines = [f"# Kernel trace of the replay study ({n} entries x {steps} steps per launch)", "",
-             "Command (repository root as $R, run from /tmp with TMPDIR=/tmp):", "",
+             "Command (repository root as $R, an output directory as $OUT, run from /tmp with TMPDIR=/tmp):", "",
              f"    {PROFILE_COMMANDS['replay_trace']}",
              f"    {PROFILE_COMMANDS['replay_trace_summary']}", "",
              "The longest call of each instance is a full-size launch: the RTN instances also run "
@@ -841,7 +841,7 @@ def summarize_valu(workload: str, pmc_dir: str) -> int:
         rows.append((_variant_of(k), _short_kernel(k), m["SQ_INSTS_VALU"] / m["SQ_WAVES"],
                      m["SQ_INSTS_VALU"] * 64 / w.entries_per_layer, busy, len(c["SQ_WAVES"])))
     lines = [f"# k_update_slab on {workload}: vector-instruction budget per launch", "",
-             "Command (repository root as $R, run from /tmp with TMPDIR=/tmp):", "",
+             "Command (repository root as $R, an output directory as $OUT, run from /tmp with TMPDIR=/tmp):", "",
              f"    {PROFILE_COMMANDS['valu']}", f"    {PROFILE_COMMANDS['valu_summary']}", "",
              f"Lane operations per entry = SQ_INSTS_VALU x 64 / {w.entries_per_layer} entries; "
              f"VALU busy = SQ_ACTIVE_INST_VALU x 4 / {simds} SIMDs / (GRBM_GUI_ACTIVE / {xcc} XCDs).",
@@ -857,24 +857,24 @@ def summarize_valu(workload: str, pmc_dir: str) -> int:
 
 
 PROFILE_COMMANDS = {
-    "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof_trace "
+    "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/prof_trace "
              "-o run -- python3 $R/bench.py",
     "fetch": "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv "
-             "-d $R/gpurun_out/prof_fetch -o run -- python3 $R/bench.py --steps 2 --warmup 1 "
+             "-d $OUT/prof_fetch -o run -- python3 $R/bench.py --steps 2 --warmup 1 "
              "--cpu-seconds 0",
     "write": "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv "
-             "-d $R/gpurun_out/prof_write -o run -- python3 $R/bench.py --steps 2 --warmup 1 "
+             "-d $OUT/prof_write -o run -- python3 $R/bench.py --steps 2 --warmup 1 "
              "--cpu-seconds 0",
-    "summary": "python3 $R/bench.py --summarize-profiles $R/gpurun_out/prof_trace "
-               "$R/gpurun_out/prof_fetch $R/gpurun_out/prof_write",
+    "summary": "python3 $R/bench.py --summarize-profiles $OUT/prof_trace "
+               "$OUT/prof_fetch $OUT/prof_write",
     "valu": "timeout -s KILL 120 rocprofv3 --pmc SQ_WAVES SQ_ACTIVE_INST_VALU SQ_WAVE_CYCLES "
             "SQ_BUSY_CYCLES SQ_INSTS_VALU GRBM_GUI_ACTIVE --output-format csv "
-            "-d $R/gpurun_out/pmc_busy -o run -- python3 $R/bench.py --steps 2 --warmup 0 "
+            "-d $OUT/pmc_busy -o run -- python3 $R/bench.py --steps 2 --warmup 0 "
             "--layers 4 --cpu-seconds 0 --no-ceiling",
-    "valu_summary": "python3 $R/bench.py --summarize-valu $R/gpurun_out/pmc_busy",
-    "replay_trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof_replay "
+    "valu_summary": "python3 $R/bench.py --summarize-valu $OUT/pmc_busy",
+    "replay_trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/prof_replay "
                     "-o run -- python3 $R/bench.py --replay --steps 4096",
-    "replay_trace_summary": "python3 $R/bench.py --summarize-trace $R/gpurun_out/prof_replay "
+    "replay_trace_summary": "python3 $R/bench.py --summarize-trace $OUT/prof_replay "
                             "k_replay.m1_long",
 }
 
