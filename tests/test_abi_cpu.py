@@ -156,3 +156,18 @@ def test_replay_validation(lib):
     # empty traces never reach the device
     assert rp(Q("weyl", "bf16"), n=0, h0=None, a=None, w=None, err=None) == 0
     assert L.ssmq_last_error() == b""
+
+
+@pytest.mark.parametrize("lang,compiler,std", [("c", "gcc", "-std=c11"), ("c++", "g++", "-std=c++17")])
+def test_header_is_self_contained(tmp_path, lang, compiler, std):
+    """include/ssmq.h compiles on its own, as C and as C++, pedantic and warning-free."""
+    import shutil
+    import subprocess
+    if shutil.which(compiler) is None:
+        pytest.skip(f"{compiler} not available")
+    src = tmp_path / "use.c"
+    src.write_text('#include "ssmq.h"\nint main(void) { return ssmq_status_string(SSMQ_OK) == 0; }\n')
+    r = subprocess.run([compiler, "-x", lang, std, "-Wall", "-Wextra", "-pedantic", "-Werror",
+                        "-fsyntax-only", "-I", os.path.dirname(HEADER), str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
