@@ -92,3 +92,60 @@ def test_conv1d_update(ssmq, batch, channels, width, act):
         mag = mag + np.abs(bias.astype(np.float64))[None]
     err = np.abs(out.cpu().numpy().astype(np.float64) - r_out)
     assert np.all(err <= 1e-5 * (mag + np.abs(r_out)) + 1e-30), err.max() if err.size else 0
+
+
+@pytest.mark.parametrize("fmt,rule,group", [("bf16", "weyl", 0), ("int8", "sr", 128)])
+def test_composed_mamba2_decode_step(ssmq, fmt, rule, group):
+    """One Mamba-2 decode step around the state (Appendix B "Runners"): the conv1d
+    update over the x, B and C channels with silu, the split into x, B, C, and the
+    fused update with dt + dt_bias, softplus and the z gate. Each stage is checked
+    against the oracle on the inputs the GPU stage actually received."""
+    b, H, P, N, G, W = 3, 8, 64, 128, 2, 4
+    di = H * P
+    ch = di + 2 * G * N
+    rng = np.random.default_rng(140)
+    conv_state = rng.standard_normal((b, ch, W)).astype(np.float32)
+    xbc = rng.standard_normal((b, ch)).astype(np.float32)
+    weight = (rng.standard_normal((ch, W)) * 0.5).astype(np.float32)
+    bias = (rng.standard_normal(ch) * 0.1).astype(np.float32)
+    dt_raw = (rng.standard_normal((b, H)) - 3).astype(np.float32)
+    dt_bias = rng.uniform(-2, 0, H).astype(np.float32)
+    z = rng.standard_normal((b, H, P)).astype(np.float32)
+    A, D = wl.layer_params("mamba2", H, N, 141)
+    codes, scale = wl.initial_state(fmt, b, H, P, N, 142, group=group)
+    say(f"case composed decode step {fmt} {rule}")
+
+    cs = torch.from_numpy(conv_state).to(DEV)
+    out = torch.empty((b, ch), device=DEV)
+    ssmq.conv1d_update(cs, torch.from_numpy(xbc).to(DEV), torch.from_numpy(weight).to(DEV),
+                       torch.from_numpy(bias).to(DEV), out, act=True)
+    x = out[:, :di].reshape(b, H, P).contiguous()
+    B = out[:, di:di + G * N].reshape(b, G, N).contiguous()
+    C = out[:, di + G * N:].reshape(b, G, N).contiguous()
+    st = codes.to(DEV)
+    sc = None if scale is None else scale.to(DEV)
+    y = torch.empty((b, H, P), device=DEV)
+    ssmq.state_update(st, sc, x, torch.from_numpy(dt_raw).to(DEV), A.to(DEV), B, C, D.to(DEV), y,
+                      rule=rule, fmt=fmt, dither_block=128, scale_group=group, step=9, layer=1,
+                      dt_bias=torch.from_numpy(dt_bias).to(DEV), dt_softplus=True,
+                      z=torch.from_numpy(z).to(DEV))
+    torch.cuda.synchronize()
+
+    r_state, r_out = oracle.conv1d_update(conv_state, xbc, weight, bias, act=True)
+    assert np.array_equal(cs.cpu().numpy(), r_state)
+    got_out = out.cpu().numpy().astype(np.float64)
+    mag = np.abs(r_state.astype(np.float64) * weight[None].astype(np.float64)).sum(-1) + np.abs(bias)
+    assert np.all(np.abs(got_out - r_out) <= 1e-5 * (mag + np.abs(r_out)))
+    xs, Bs, Cs = (v.cpu().numpy() for v in (x, B, C))
+    r_codes, r_scale, r_y, r_h = oracle.state_update(
+        fmt, rule, wl.to_numpy_codes(fmt, codes), None if scale is None else scale.numpy(), xs,
+        dt_raw, A.numpy(), Bs, Cs, D.numpy(), step=9, layer=1, block=128, group=group,
+        dt_bias=dt_bias, dt_softplus=True, z=z)
+    assert_codes(fmt, wl.to_numpy_codes(fmt, st.cpu()), r_codes, "composed step")
+    if sc is not None:
+        np.testing.assert_array_equal(sc.cpu().numpy(), r_scale)
+    Ch = np.repeat(Cs.astype(np.float64), H // G, axis=1)[:, :, None, :]
+    mag = (np.abs(Ch * r_h.astype(np.float64)).sum(-1) + np.abs(D.numpy()[None, :, None] * xs))
+    mag = mag * np.abs(torch.nn.functional.silu(torch.from_numpy(z).double()).numpy())
+    err = np.abs(y.cpu().numpy().astype(np.float64) - r_y)
+    assert np.all(err <= 1e-5 * (mag + np.abs(r_y)) + 1e-30), err.max()
