@@ -335,8 +335,9 @@ __device__ inline uint32_t round_code(float x, uint32_t thr) {
 }
 
 // ---------------------------------------------------------------------------
-// Chunk quantizers: V fp32 values (E4M3: already multiplied by 1/scale) -> one
-// 16-byte chunk of codes, fast path plus the exact path for rare entries.
+// Chunk quantizers: one chunk of fp32 values -> its codes, fast path plus the
+// exact path for rare entries (the unscaled float formats here, E4M3 and the
+// integer formats, which also take the group's 1 / s, further below).
 // ---------------------------------------------------------------------------
 template <int F>
 __device__ inline void patch_code(uint32_t (&w)[4], int k, uint32_t c) {
@@ -364,20 +365,17 @@ __device__ inline bool needs_exact_path(float v) {
   }
 }
 
-// Does any value of the chunk need the exact path? maybe_nan comes from the
-// caller (a NaN anywhere in the chunk, possibly a false alarm); the small-
-// magnitude tests use the chunk minimum (fminf ignores NaN).
+// Does any value of the chunk need the exact path (fp16 below its normal range)?
+// The small-magnitude test uses the chunk minimum (fminf ignores NaN).
 template <int F, int R, int V>
-__device__ inline bool chunk_is_rare(const float (&v)[V], bool maybe_nan) {
-  if constexpr (F == kBF16 || F == kFP32) return false;
-  else if constexpr (F == kFP16 && R == kRTN) return false;
-  else if constexpr (F == kE4M3 && R == kRTN) return maybe_nan;
-  else {
+__device__ inline bool chunk_is_rare(const float (&v)[V]) {
+  if constexpr (F != kFP16 || R == kRTN) {
+    return false;
+  } else {
     float mn = __builtin_fabsf(v[0]);
 #pragma unroll
     for (int k = 1; k < V; ++k) mn = fminf(mn, __builtin_fabsf(v[k]));
-    if constexpr (F == kFP16) return mn < 0x1p-14f;
-    else return maybe_nan || !(mn >= 0x1p-10f);
+    return mn < 0x1p-14f;
   }
 }
 
@@ -390,9 +388,11 @@ __device__ inline bool chunk_has_nan(const float (&v)[V]) {
   return n;
 }
 
+// The unscaled float formats need no NaN test: their conversions give the
+// canonical NaN (maybe_nan is accepted for a uniform interface).
 template <int F, int R, typename TG>
 __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG& tg,
-                                       bool maybe_nan) {
+                                       bool /*maybe_nan*/) {
   static_assert(F == kBF16 || F == kFP16 || F == kFP32, "unscaled float formats");
   uint32_t w[4];
   if constexpr (F == kFP32) {
@@ -431,7 +431,7 @@ __device__ inline uint4 quantize_chunk(const float (&v)[Traits<F>::V], const TG&
       w[i] = __builtin_bit_cast(uint32_t, p);
     }
   }
-  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, Traits<F>::V>(v, maybe_nan)) != 0) {
+  if (__builtin_amdgcn_ballot_w64(chunk_is_rare<F, R, Traits<F>::V>(v)) != 0) {
 #pragma unroll
     for (int k = 0; k < Traits<F>::V; ++k) {
       if (needs_exact_path<F, R>(v[k])) patch_code<F>(w, k, round_code<F, R>(v[k], tg(k)));

@@ -12,15 +12,17 @@
 //   k_requant      fp32 -> codes for fp16 / bf16 / fp32, one chunk per thread.
 //   k_requant_scaled fp32 -> E4M3 / INT8 / INT4 codes with group scales.
 //   k_dither_fill  the 24-bit thresholds themselves.
+//   k_conv1d_update the causal depthwise convolution's decode step.
 //   k_replay       open-loop replay of recorded decays and writes: a reference
 //                  and a stored trajectory per entry, iterated in registers.
 //
-// Layout. A chunk is 16 bytes of codes: V = 8 (fp16, bf16), 16 (E4M3) or 4
-// (fp32) consecutive entries of one state row. The LR = dstate / V chunks of a
-// row sit in LR consecutive lanes of one wave, so a lane's slice of B and C is
-// fixed and C.h is an LR-lane reduction. Each thread owns CPT chunks (one row
-// per pass); the state moves with nontemporal 16-byte accesses, which on this
-// chip stream an in-place read-modify-write fastest with one chunk per thread.
+// Layout. A chunk is the codes of V consecutive entries of one state row: 16
+// bytes holding 8 fp16 / bf16, 16 E4M3 / INT8 or 4 fp32 entries, or 8 bytes
+// holding 16 INT4 entries. The LR = dstate / V chunks of a row sit in LR
+// consecutive lanes of one wave, so a lane's slice of B and C is fixed and C.h
+// is an LR-lane reduction. Each thread owns CPT chunks (one row per pass); the
+// state moves with nontemporal 16- or 8-byte accesses (each byte is touched once
+// per step, so nothing is gained by keeping it in the caches).
 #include "ssmq_device.hpp"
 
 namespace ssmq {
@@ -128,13 +130,21 @@ void k_update_slab(UpdateArgs a) {
 
   float h[CPT][V];
   bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
+  // Scaled formats store v * s_old; dA * (v * s_old) is evaluated as
+  // fma(fl32(dA * s_old), v, w). E4M3 reads a head-wide scale once, before the
+  // loop (read inside it, the load is repeated after each chunk's y store); the
+  // INT kernels measure faster with one select-addressed load per chunk.
+  float dA_head = dA;
+  if constexpr (F == kE4M3)
+    if (a.lanes_per_group == 0) dA_head = dA * a.scale[tile];
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    // Scaled formats store v * s_old; dA * (v * s_old) is evaluated as
-    // fma(fl32(dA * s_old), v, w).
-    float dAj = dA;
-    if constexpr (Traits<F>::scaled)
+    float dAj = dA_head;
+    if constexpr (F == kE4M3) {
+      if (a.lanes_per_group != 0) dAj = dA * a.scale[(e0 + j * pass) >> a.group_shift];
+    } else if constexpr (Traits<F>::scaled) {
       dAj = dA * ((a.lanes_per_group == 0) ? a.scale[tile] : a.scale[(e0 + j * pass) >> a.group_shift]);
+    }
     float hp[V];
     decode_chunk<F>(raw[j], hp);
     const float dx = dtv * xv[j];
