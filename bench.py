@@ -907,12 +907,12 @@ def cpu_baseline(w, variant, target_s):
         return time.perf_counter() - t0
 
     probe_heads = w.nheads // w.ngroups   # the heads of one B/C group
-    t_probe = run(probe_heads)
-    per_head = t_probe / probe_heads
-    reps = max(1, int(target_s / max(t_probe, 1e-6)))
-    total = 0.0
-    for _ in range(reps):
+    run(probe_heads)                       # first call: loading and first-touch costs
+    reps, total = 0, 0.0
+    while total < target_s:
         total += run(probe_heads)
+        reps += 1
+    per_head = total / (reps * probe_heads)
     entries = reps * probe_heads * P * N
     bytes_rw = entries * state_bytes_per_entry(fmt) * 2
     return {
