@@ -64,6 +64,8 @@ def parse_args():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="seconds of each oracle baseline leg, one thread and all cores (0 disables it)")
+    ap.add_argument("--rounds", type=int, default=1,
+                    help="timed regions per variant, interleaved across variants; the median is reported")
     ap.add_argument("--graph", action="store_true",
                     help="replay the timed steps from one HIP graph (removes host launch gaps)")
     ap.add_argument("--no-ceiling", action="store_true",
@@ -110,6 +112,9 @@ def main() -> int:
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this benchmark measures one GPU only; the state update shards "
                                    "by batch or head with no communication, so --gpus must be 1"}))
+        return 2
+    if args.rounds < 1:
+        print(json.dumps({"error": "--rounds must be at least 1"}))
         return 2
 
     import torch
@@ -168,7 +173,11 @@ def main() -> int:
     results = {}
     t_global = 1
     launches = args.steps * L
-    for fmt, rule in variants:
+    round_ms = {f"{fmt}:{rule}": [] for fmt, rule in variants}
+
+    def timed_region(fmt, rule):
+        """Warm-up steps, then exactly --steps timed steps; returns the region's ms."""
+        nonlocal t_global
         for _ in range(args.warmup):
             one_step(fmt, rule, t_global)
             t_global += 1
@@ -198,7 +207,17 @@ def main() -> int:
                 t_global += 1
             stop.record(stream)
         torch.cuda.synchronize()
-        total_ms = start.elapsed_time(stop)
+        return start.elapsed_time(stop)
+
+    # --rounds R > 1 interleaves the variants round by round and keeps each
+    # variant's median round (the paper's kernel table takes the median of seven
+    # interleaved rounds); one round is one timed region per variant.
+    for _ in range(args.rounds):
+        for fmt, rule in variants:
+            round_ms[f"{fmt}:{rule}"].append(timed_region(fmt, rule))
+    for fmt, rule in variants:
+        rounds = sorted(round_ms[f"{fmt}:{rule}"])
+        total_ms = rounds[len(rounds) // 2]
         ms_step = total_ms / args.steps
         avg_launch_ms = total_ms / launches
         # Diagnostic only: one more step with events around every launch (each pair
@@ -221,6 +240,8 @@ def main() -> int:
                                           "min": 1e3 * min(per_launch),
                                           "max": 1e3 * max(per_launch)},
         }
+        if args.rounds > 1:
+            results[f"{fmt}:{rule}"]["rounds_kernel_avg_us"] = [1e3 * r / launches for r in round_ms[f"{fmt}:{rule}"]]
 
     # ---- streaming ceiling: a plain elementwise kernel of known size ----------------
     # torch.neg over 1 GiB of fp32 reads 1 GiB and writes 1 GiB; it is also the
