@@ -60,7 +60,7 @@ def parse_args():
                                           "e4m3:weyl,e4m3:sr,e4m3:rtn,e4m3:philox,"
                                           "int8:weyl,int8:sr,int8:rtn,int8:philox,"
                                           "int4:weyl,int4:sr,int4:rtn",
-                    help="comma-separated format:rule list; the first is the headline")
+                    help="comma-separated format[/group]:rule list (group: entries per scale, 0 = one per head); the first is the headline")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="seconds of each oracle baseline leg, one thread and all cores (0 disables it)")
@@ -86,16 +86,32 @@ def state_bytes_per_entry(fmt: str) -> float:
     return {"bf16": 2, "fp16": 2, "e4m3": 1, "fp32": 4, "int8": 1, "int4": 0.5}[fmt]
 
 
-def state_bytes_per_launch(w, fmt: str) -> int:
+def state_bytes_per_launch(w, fmt: str, group=None) -> int:
     """Algorithmic bytes of one layer's update: codes read and written, plus each
-    group scale read and written (4 B each way)."""
+    group scale read and written (4 B each way). group: entries per scale (0 = one
+    head; None = the workload's own)."""
     from paper_2609_39185_amd import workloads as wl
 
     n = w.entries_per_layer
     total = int(n * state_bytes_per_entry(fmt) * 2)
     if fmt in ("e4m3", "int8", "int4"):
-        total += (n // (wl.scale_group_of(w, fmt) or w.headdim * w.dstate)) * 8
+        if group is None:
+            group = wl.scale_group_of(w, fmt)
+        total += (n // (group or w.headdim * w.dstate)) * 8
     return total
+
+
+def parse_variant(spec: str, w):
+    """'fmt:rule' or 'fmt/group:rule' (group: entries per scale of a scaled format,
+    0 = one per head) -> dict(key, fmt, rule, group)."""
+    from paper_2609_39185_amd import workloads as wl
+
+    head, rule = spec.split(":")
+    fmt, _, g = head.partition("/")
+    if g and fmt not in ("e4m3", "int8", "int4"):
+        raise SystemExit(f"variant {spec}: only e4m3, int8 and int4 take a scale group")
+    group = int(g) if g else wl.scale_group_of(w, fmt)
+    return {"key": spec, "fmt": fmt, "rule": rule, "group": group}
 
 
 def main() -> int:
@@ -141,8 +157,8 @@ def main() -> int:
     L = args.layers or w.layers
     b, H, P, N, G = w.batch, w.nheads, w.headdim, w.dstate, w.ngroups
     n_entries = w.entries_per_layer
-    variants = [tuple(v.split(":")) for v in args.variants.split(",") if v]
-    fmts = sorted({f for f, _ in variants})
+    variants = [parse_variant(v, w) for v in args.variants.split(",") if v]
+    stored = sorted({(v["fmt"], v["group"]) for v in variants})
 
     # ---- resident inputs and states -------------------------------------------------
     layers = []
@@ -151,35 +167,34 @@ def main() -> int:
         x, dt, B, C = wl.step_inputs(b, H, P, N, G, seed=2000 + ell, device=dev)
         y = torch.empty((b, H, P), dtype=torch.float32, device=dev)
         states = {}
-        for f in fmts:
-            states[f] = wl.initial_state(f, b, H, P, N, seed=3000 + ell,
-                                         group=wl.scale_group_of(w, f), device=dev)
+        for f, g in stored:
+            states[(f, g)] = wl.initial_state(f, b, H, P, N, seed=3000 + ell, group=g, device=dev)
         layers.append(dict(A=A, D=D, x=x, dt=dt, B=B, C=C, y=y, states=states))
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream(dev)
 
-    def one_step(fmt, rule, t, events=None, on=None):
+    def one_step(var, t, events=None, on=None):
         for ell, lay in enumerate(layers):
-            st, sc = lay["states"][fmt]
+            st, sc = lay["states"][(var["fmt"], var["group"])]
             if events is not None:
                 events[ell][0].record(stream)
             ssmq.state_update(st, sc, lay["x"], lay["dt"], lay["A"], lay["B"], lay["C"], lay["D"],
-                              lay["y"], rule=rule, fmt=fmt, dither_block=w.dither_block,
-                              scale_group=wl.scale_group_of(w, fmt), layer=ell, step=t, seed=0,
-                              stream=on or stream)
+                              lay["y"], rule=var["rule"], fmt=var["fmt"],
+                              dither_block=w.dither_block, scale_group=var["group"], layer=ell,
+                              step=t, seed=0, stream=on or stream)
             if events is not None:
                 events[ell][1].record(stream)
 
     results = {}
     t_global = 1
     launches = args.steps * L
-    round_ms = {f"{fmt}:{rule}": [] for fmt, rule in variants}
+    round_ms = {v["key"]: [] for v in variants}
 
-    def timed_region(fmt, rule):
+    def timed_region(var):
         """Warm-up steps, then exactly --steps timed steps; returns the region's ms."""
         nonlocal t_global
         for _ in range(args.warmup):
-            one_step(fmt, rule, t_global)
+            one_step(var, t_global)
             t_global += 1
         torch.cuda.synchronize()
         # Timed region: exactly --steps steps between two events on the launch stream.
@@ -194,7 +209,7 @@ def main() -> int:
             with torch.cuda.graph(graph):
                 cap = torch.cuda.current_stream(dev)
                 for k in range(args.steps):
-                    one_step(fmt, rule, t_global + k, on=cap)
+                    one_step(var, t_global + k, on=cap)
             torch.cuda.synchronize()
             start.record(stream)
             graph.replay()
@@ -203,7 +218,7 @@ def main() -> int:
         else:
             start.record(stream)
             for k in range(args.steps):
-                one_step(fmt, rule, t_global)
+                one_step(var, t_global)
                 t_global += 1
             stop.record(stream)
         torch.cuda.synchronize()
@@ -213,22 +228,23 @@ def main() -> int:
     # variant's median round (the paper's kernel table takes the median of seven
     # interleaved rounds); one round is one timed region per variant.
     for _ in range(args.rounds):
-        for fmt, rule in variants:
-            round_ms[f"{fmt}:{rule}"].append(timed_region(fmt, rule))
-    for fmt, rule in variants:
-        rounds = sorted(round_ms[f"{fmt}:{rule}"])
+        for var in variants:
+            round_ms[var["key"]].append(timed_region(var))
+    for var in variants:
+        key = var["key"]
+        rounds = sorted(round_ms[key])
         total_ms = rounds[len(rounds) // 2]
         ms_step = total_ms / args.steps
         avg_launch_ms = total_ms / launches
         # Diagnostic only: one more step with events around every launch (each pair
         # adds a few microseconds, so these durations run long).
         ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(L)]]
-        one_step(fmt, rule, t_global, ev[0])
+        one_step(var, t_global, ev[0])
         t_global += 1
         torch.cuda.synchronize()
         per_launch = [e[0].elapsed_time(e[1]) for e in ev[0]]
-        sbytes = state_bytes_per_launch(w, fmt)
-        results[f"{fmt}:{rule}"] = {
+        sbytes = state_bytes_per_launch(w, var["fmt"], var["group"])
+        results[key] = {
             "ms_per_step": ms_step,
             "steps_per_s": 1000.0 / ms_step,
             "state_GBps": sbytes * L / (ms_step * 1e6),
@@ -241,7 +257,7 @@ def main() -> int:
                                           "max": 1e3 * max(per_launch)},
         }
         if args.rounds > 1:
-            results[f"{fmt}:{rule}"]["rounds_kernel_avg_us"] = [1e3 * r / launches for r in round_ms[f"{fmt}:{rule}"]]
+            results[key]["rounds_kernel_avg_us"] = [1e3 * r / launches for r in round_ms[key]]
 
     # ---- streaming ceiling: a plain elementwise kernel of known size ----------------
     # torch.neg over 1 GiB of fp32 reads 1 GiB and writes 1 GiB; it is also the
@@ -271,8 +287,9 @@ def main() -> int:
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(w, variants[0], args.cpu_seconds)
 
-    head_fmt, head_rule = variants[0]
-    head = results[f"{head_fmt}:{head_rule}"]
+    head_var = variants[0]
+    head_fmt, head_rule = head_var["fmt"], head_var["rule"]
+    head = results[head_var["key"]]
     measured = load_traffic(w.name)
     for key, r in results.items():
         t = measured.get(key) if measured else None
@@ -305,7 +322,7 @@ def main() -> int:
         "config": {"workload": w.name, "family": w.family, "batch": b, "layers": L, "nheads": H,
                    "headdim": P, "dstate": N, "ngroups": G, "format": head_fmt,
                    "rule": head_rule, "dither_block": w.dither_block,
-                   "scale_group": (wl.scale_group_of(w, head_fmt) or P * N)
+                   "scale_group": (head_var["group"] or P * N)
                    if head_fmt in ("e4m3", "int8", "int4") else None,
                    "launch": "hip_graph" if args.graph else "stream"},
         "pct_of_peak": head["pct_of_peak"],
@@ -908,12 +925,11 @@ def cpu_baseline(w, variant, target_s):
     import oracle
     from paper_2609_39185_amd import workloads as wl
 
-    fmt, rule = variant
+    fmt, rule, group = variant["fmt"], variant["rule"], variant["group"]
     P, N = w.headdim, w.dstate
     A, D = wl.layer_params(w.family, w.nheads, N, seed=1000)
     x, dt, B, C = wl.step_inputs(1, w.nheads, P, N, w.ngroups, seed=2000)
-    codes, scale = wl.initial_state(fmt, 1, w.nheads, P, N, seed=3000,
-                                    group=wl.scale_group_of(w, fmt))
+    codes, scale = wl.initial_state(fmt, 1, w.nheads, P, N, seed=3000, group=group)
     codes_np = wl.to_numpy_codes(fmt, codes)
     args = (None if scale is None else scale.numpy(), x.numpy(), dt.numpy(), A.numpy(),
             B.numpy(), C.numpy(), D.numpy())
@@ -924,7 +940,7 @@ def cpu_baseline(w, variant, target_s):
         t0 = time.perf_counter()
         oracle.state_update(fmt, rule, c, sc, args[1][:, :nh], args[2][:, :nh], args[3][:nh],
                             args[4][:, :1], args[5][:, :1], args[6][:nh], block=w.dither_block,
-                            group=wl.scale_group_of(w, fmt), step=1)
+                            group=group, step=1)
         return time.perf_counter() - t0
 
     probe_heads = w.nheads // w.ngroups   # the heads of one B/C group

@@ -81,3 +81,20 @@ def test_replay_trace_summary_rates(tmp_path, monkeypatch):
     # 8 B x 1,310,720 entries x 4096 steps in 10 ms
     assert "int8:weyl" in row and row.rstrip(" |").endswith(f"{8 * 1310720 * 4096 / 1e7:.0f}")
     assert "other_kernel" not in text
+
+
+def test_variant_specs_and_their_algorithmic_bytes():
+    from paper_2609_39185_amd import workloads as wl
+    w = wl.WORKLOADS["hybrid_m2_stack"]
+    n = w.entries_per_layer
+    v = bench.parse_variant("e4m3:weyl", w)
+    assert (v["fmt"], v["rule"], v["group"]) == ("e4m3", "weyl", wl.scale_group_of(w, "e4m3"))
+    # one scale per 64x128 head: codes 1 B each way, scale 4 B each way per head
+    assert bench.state_bytes_per_launch(w, "e4m3", 0) == 2 * n + 8 * (n // 8192)
+    v = bench.parse_variant("e4m3/128:sr", w)
+    assert (v["key"], v["fmt"], v["rule"], v["group"]) == ("e4m3/128:sr", "e4m3", "sr", 128)
+    assert bench.state_bytes_per_launch(w, "e4m3", 128) == 2 * n + 8 * (n // 128)
+    assert bench.state_bytes_per_launch(w, "int4", 16) == n + 8 * (n // 16)
+    assert bench.state_bytes_per_launch(w, "bf16") == 4 * n
+    with pytest.raises(SystemExit):
+        bench.parse_variant("bf16/128:weyl", w)
