@@ -54,9 +54,9 @@ __device__ inline float silu(float v) { return v / (1.0f + expf(-v)); }
 // Mamba-2 head slabs: NT threads x CPT chunks = a run of whole rows of one head.
 // ---------------------------------------------------------------------------
 // The whole-head configurations of the scaled formats (four chunks per thread,
-// up to 128 threads) hold 64 state values per thread and sit at the 128-register
-// line; they are held to it (four waves per SIMD), at the price of a few bytes
-// of spilled addresses, instead of dropping to three waves.
+// up to 128 threads) hold 64 state values per thread and sit near the
+// 128-register line; they are held to it (four waves per SIMD) instead of
+// dropping to three waves.
 //
 // N128: the state dimension is 128 and a scale group is 128 entries (8 lanes)
 // or the whole head, so the lanes per row and per group are compile-time
@@ -131,20 +131,28 @@ void k_update_slab(UpdateArgs a) {
   float h[CPT][V];
   bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
   // Scaled formats store v * s_old; dA * (v * s_old) is evaluated as
-  // fma(fl32(dA * s_old), v, w). E4M3 reads a head-wide scale once, before the
-  // loop (read inside it, the load is repeated after each chunk's y store); the
-  // INT kernels measure faster with one select-addressed load per chunk.
-  float dA_head = dA;
-  if constexpr (F == kE4M3)
-    if (a.lanes_per_group == 0) dA_head = dA * a.scale[tile];
+  // fma(fl32(dA * s_old), v, w). E4M3 reads its scales before the loop (read
+  // inside it, each load is issued after the previous chunk's y store to LDS
+  // and waited for at once); the INT kernels measure faster with one
+  // select-addressed load per chunk.
+  float dAs[CPT];
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) dAs[j] = dA;
+  if constexpr (F == kE4M3) {
+    if (a.lanes_per_group == 0) {
+      const float d = dA * a.scale[tile];
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) dAs[j] = d;
+    } else {
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) dAs[j] = dA * a.scale[(e0 + j * pass) >> a.group_shift];
+    }
+  }
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
-    float dAj = dA_head;
-    if constexpr (F == kE4M3) {
-      if (a.lanes_per_group != 0) dAj = dA * a.scale[(e0 + j * pass) >> a.group_shift];
-    } else if constexpr (Traits<F>::scaled) {
+    float dAj = dAs[j];
+    if constexpr (is_int_fmt<F>)
       dAj = dA * ((a.lanes_per_group == 0) ? a.scale[tile] : a.scale[(e0 + j * pass) >> a.group_shift]);
-    }
     float hp[V];
     decode_chunk<F>(raw[j], hp);
     const float dx = dtv * xv[j];
