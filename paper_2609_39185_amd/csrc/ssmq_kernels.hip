@@ -131,14 +131,16 @@ void k_update_slab(UpdateArgs a) {
   float h[CPT][V];
   bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
   // Scaled formats store v * s_old; dA * (v * s_old) is evaluated as
-  // fma(fl32(dA * s_old), v, w). E4M3 reads its scales before the loop (read
-  // inside it, each load is issued after the previous chunk's y store to LDS
-  // and waited for at once); the INT kernels measure faster with one
-  // select-addressed load per chunk.
+  // fma(fl32(dA * s_old), v, w). E4M3, and the four-chunk configurations (one
+  // scale per head), read their scales before the loop (read inside it, each
+  // load is issued after the previous chunk's y store and waited for at once);
+  // the block-scaled INT kernels measure faster with one select-addressed load
+  // per chunk.
+  constexpr bool kScalesFirst = (F == kE4M3) || (is_int_fmt<F> && CPT >= 4);
   float dAs[CPT];
 #pragma unroll
   for (int j = 0; j < CPT; ++j) dAs[j] = dA;
-  if constexpr (F == kE4M3) {
+  if constexpr (kScalesFirst) {
     if (a.lanes_per_group == 0) {
       const float d = dA * a.scale[tile];
 #pragma unroll
@@ -151,7 +153,7 @@ void k_update_slab(UpdateArgs a) {
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
     float dAj = dAs[j];
-    if constexpr (is_int_fmt<F>)
+    if constexpr (is_int_fmt<F> && !kScalesFirst)
       dAj = dA * ((a.lanes_per_group == 0) ? a.scale[tile] : a.scale[(e0 + j * pass) >> a.group_shift]);
     float hp[V];
     decode_chunk<F>(raw[j], hp);
