@@ -130,6 +130,7 @@ void k_update_slab(UpdateArgs a) {
 
   float h[CPT][V];
   bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
+  float yo[CPT];  // rows' y, for kernels that store it directly
   // Scaled formats store v * s_old; dA * (v * s_old) is evaluated as
   // fma(fl32(dA * s_old), v, w). E4M3, and the four-chunk configurations (one
   // scale per head), read their scales before the loop (read inside it, each
@@ -177,11 +178,18 @@ void k_update_slab(UpdateArgs a) {
     }
     bad[j] = !__builtin_isfinite(ys);
     ys = lane_sum(ys, lanes_per_row);
+    if constexpr (kStageY) {
+      if (cc == 0) sY[(t >> lr_shift) + j * rows_per_pass] = ys + Dv * xv[j];
+    } else {
+      yo[j] = ys + Dv * xv[j];
+    }
+  }
+  if constexpr (!kStageY) {
+    // Stored after the loop, so no chunk's scale load waits behind a y store.
     if (cc == 0) {
-      if constexpr (kStageY) {
-        sY[(t >> lr_shift) + j * rows_per_pass] = ys + Dv * xv[j];
-      } else {
-        float yv = ys + Dv * xv[j];
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        float yv = yo[j];
         if (a.z) yv = yv * silu(a.z[tile * a.headdim + r0 + j * rows_per_pass]);
         hy[r0 + j * rows_per_pass] = yv;
       }
