@@ -93,19 +93,10 @@ void k_update_slab(UpdateArgs a) {
   const uint32_t pass = static_cast<uint32_t>(rows_per_pass * a.dstate);  // entries per pass
   const int64_t e0 = tile_base + l0;
 
-  chunk_t<F> raw[CPT];
-  float xv[CPT];
-#pragma unroll
-  for (int j = 0; j < CPT; ++j) {
-    raw[j] = load_stream<chunk_t<F>>(hstate + chunk_bytes_at<F>(l0 + j * pass));
-    xv[j] = hx[r0 + j * rows_per_pass];
-  }
-  const float dt_in = a.dt[tile];
-  const float Dv = a.D ? a.D[hh] : 0.0f;
-
   // Per-head values are staged once per workgroup in LDS while the state loads
-  // are in flight: B and C of the head's group (one float4 per thread), and
-  // exp(dt A), evaluated by the first wave in double with one final rounding.
+  // are in flight: B and C of the head's group (one float4 per thread, loaded
+  // before the state so that staging them waits for them alone), and exp(dt A),
+  // evaluated by the first wave in double with one final rounding.
   __shared__ float4 sBC[kMaxDstate / 2];
   __shared__ float sh[4];
   // y of the slab is staged here and written back as whole lines (the integer
@@ -116,13 +107,32 @@ void k_update_slab(UpdateArgs a) {
   const int nq = a.dstate >> 2;  // float4 per vector
   const float* Bg = a.B + (b * a.ngroups + g) * a.dstate;
   const float* Cg = a.C + (b * a.ngroups + g) * a.dstate;
-  for (int i = t; i < 2 * nq; i += NT)
-    sBC[i] = (i < nq) ? reinterpret_cast<const float4*>(Bg)[i]
-                      : reinterpret_cast<const float4*>(Cg)[i - nq];
+  const bool bc_one = 2 * nq <= NT;  // one float4 of B or C per thread at most
+  float4 bc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  if (bc_one && t < 2 * nq)
+    bc = (t < nq) ? reinterpret_cast<const float4*>(Bg)[t] : reinterpret_cast<const float4*>(Cg)[t - nq];
+
+  chunk_t<F> raw[CPT];
+  float xv[CPT];
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    raw[j] = load_stream<chunk_t<F>>(hstate + chunk_bytes_at<F>(l0 + j * pass));
+    xv[j] = hx[r0 + j * rows_per_pass];
+  }
+  const float dt_in = a.dt[tile];
+  const float Dv = a.D ? a.D[hh] : 0.0f;
+
   if (t < 64) {
     const float dte = step_size(a, dt_in, hh);
     const float d = decay(dte, a.A[hh]);
     if (t == 0) { sh[0] = d; sh[2] = dte; sDone = 0; }
+  }
+  if (bc_one) {
+    if (t < 2 * nq) sBC[t] = bc;
+  } else {
+    for (int i = t; i < 2 * nq; i += NT)
+      sBC[i] = (i < nq) ? reinterpret_cast<const float4*>(Bg)[i]
+                        : reinterpret_cast<const float4*>(Cg)[i - nq];
   }
   __syncthreads();
   const float dA = sh[0];
