@@ -216,6 +216,12 @@ ssmq_status ssmq_state_update_ex(const ssmq_dims* dims, const ssmq_qparams* q,
     a.slabs_per_head = static_cast<int32_t>(
         head_chunks / (ssmq::kSlabThreads[cfg] * ssmq::kSlabChunks[cfg]));
     a.lanes_per_group = scaled ? static_cast<int32_t>(group / 16) : 1;
+    // E4M3 block scales: four chunks per thread as with one scale per head
+    // (measured 4-8 % faster; the INT kernels measure slower that way).
+    if (q->format == SSMQ_FP8_E4M3 && head_chunks % 512 == 0) {
+      cfg = ssmq::kSlab128x4;
+      a.slabs_per_head = static_cast<int32_t>(head_chunks / 512);
+    }
   }
   if (cfg >= 0)
     a.n128 = (d.dstate == 128 && (!scaled || a.lanes_per_group == 0 || a.lanes_per_group == 8)) ? 1 : 0;
