@@ -283,13 +283,14 @@ def test_proposition1_through_the_kernel(ssmq):
 # --------------------------------------------------------------------------
 # full-size workloads, sampled tiles against the oracle
 # --------------------------------------------------------------------------
-def _full_size_sampled(ssmq, name, fmt, rule, n_tiles=24):
+def _full_size_sampled(ssmq, name, fmt, rule, n_tiles=24, group=None):
     """One full-size layer in the launch configuration the bench times; sampled head
-    tiles against the oracle (codes within the bar, scales exact, y within 1e-5)."""
+    tiles against the oracle (codes within the bar, scales exact, y within 1e-5).
+    group: entries per scale (0 = one per head; None = the workload's own)."""
     import paper_2609_39185_amd as m
     w = wl.WORKLOADS[name]
     b, H, P, N, G = w.batch, w.nheads, w.headdim, w.dstate, w.ngroups
-    grp = wl.scale_group_of(w, fmt)
+    grp = wl.scale_group_of(w, fmt) if group is None else group
     per_tile = (P * N) // (grp or P * N) if fmt in oracle.SCALED else 0
     say(f"case full size {name} {fmt} {rule} group {grp}: {w.entries_per_layer} entries")
     A, D = wl.layer_params(w.family, H, N, 500, device=DEV)
@@ -337,6 +338,15 @@ BENCH_VARIANTS += [("int4", r) for r in ("weyl", "sr", "rtn")]
 def test_full_size_hybrid_stack_layer(ssmq, fmt, rule):
     """Every format and rule the bench reports, at the bench's layer shape."""
     _full_size_sampled(ssmq, "hybrid_m2_stack", fmt, rule)
+
+
+@pytest.mark.parametrize("fmt,rule,group", [("e4m3", "weyl", 128), ("e4m3", "rtn", 16),
+                                            ("e4m3", "sr", 256), ("int8", "weyl", 16),
+                                            ("int8", "weyl", 0), ("int4", "rtn", 0),
+                                            ("int4", "sr", 16)])
+def test_full_size_hybrid_layer_other_groups(ssmq, fmt, rule, group):
+    """The scale groups timed beside the bench's own (bench.py --variants fmt/group:rule)."""
+    _full_size_sampled(ssmq, "hybrid_m2_stack", fmt, rule, group=group)
 
 
 def test_full_size_fp8_decode(ssmq):
