@@ -651,7 +651,11 @@ __device__ inline float group_scale(float m) {
   float s = fmaf(m, Traits<F>::zh, m * Traits<F>::zl);
   const bool slow = !(m >= 0x1p-112f && m <= 3.40282347e38f);
   if (__builtin_amdgcn_ballot_w64(slow) != 0) {
-    if (slow) s = m / Traits<F>::qmax;
+    // The empty asm keeps the division inside the branch: hoisted out of it
+    // (the compiler's choice for a cheap-looking fdiv), every group pays for it.
+    float mm = m;
+    asm volatile("" : "+v"(mm));
+    if (slow) s = mm / Traits<F>::qmax;
   }
   return (s >= 1.17549435e-38f) ? s : 0.0f;
 }
