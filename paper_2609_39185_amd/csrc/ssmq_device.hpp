@@ -520,10 +520,12 @@ __device__ inline chunk_t<F> quantize_int_chunk(const float (&h)[16], float r, f
   uint32_t S[16];
   bool rare = maybe_nan;
   if constexpr (R == kRTN) {
+    // Adding 1.5 * 2^23 rounds the clamped q to an integer, ties to even (the
+    // sum's ulp is 1), and leaves that integer's two's complement in the low
+    // bits of the sum's encoding.
 #pragma unroll
     for (int k = 0; k < 16; ++k)
-      S[k] = static_cast<uint32_t>(static_cast<int>(
-          __builtin_rintf(__builtin_amdgcn_fmed3f(h[k] * r, -qmax, qmax))));
+      S[k] = __float_as_uint(__builtin_amdgcn_fmed3f(h[k] * r, -qmax, qmax) + 0x1.8p23f);
   } else {
     float mn = __builtin_inff();
 #pragma unroll
