@@ -259,13 +259,25 @@ void k_update_slab(UpdateArgs a) {
     }
   }
 
-  const uint32_t base0 = thr_base<R>(a.entry_base + static_cast<uint64_t>(e0), a.thr);
+  // Threshold bases of the chunks: one pass of NT chunks apart, a constant
+  // step when the pass spans whole dither blocks. The direct form is kept
+  // inside its branch by the empty asm: if-converted, its two 32-bit
+  // multiplies would run for every chunk.
+  uint32_t bases[CPT];
+  bases[0] = thr_base<R>(a.entry_base + static_cast<uint64_t>(e0), a.thr);
+  if (a.pass_thr_ok) {
+#pragma unroll
+    for (int j = 1; j < CPT; ++j) bases[j] = bases[0] + static_cast<uint32_t>(j) * a.pass_thr_inc;
+  } else {
+    uint64_t eb = a.entry_base + static_cast<uint64_t>(e0);
+    asm volatile("" : "+v"(eb));
+#pragma unroll
+    for (int j = 1; j < CPT; ++j) bases[j] = thr_base<R>(eb + static_cast<uint64_t>(j) * pass, a.thr);
+  }
 #pragma unroll
   for (int j = 0; j < CPT; ++j) {
     const int64_t e = e0 + static_cast<int64_t>(j) * pass;
-    const uint32_t base = (j == 0) ? base0
-                          : (a.pass_thr_ok ? base0 + static_cast<uint32_t>(j) * a.pass_thr_inc
-                                           : thr_base<R>(a.entry_base + static_cast<uint64_t>(e), a.thr));
+    const uint32_t base = bases[j];
     const chunk_t<F> out = quantize_any<F, R>(
         h[j], r[j], chunk_thr<R, V>(a.entry_base + static_cast<uint64_t>(e), a.thr, base, a.toff),
         bad[j], clamp);
