@@ -50,6 +50,9 @@ def parse_args():
                     help="--state-error: decay-rate recipe")
     ap.add_argument("--se-cc", type=int, default=0,
                     help="--state-error: also run checkpointed rules, rounding every k-th write")
+    ap.add_argument("--entry-points", action="store_true",
+                    help="instead of the fused step: ssmq_requantize and ssmq_dither_fill on one "
+                         "layer's entries (GB/s of their own reads and writes)")
     ap.add_argument("--replay", action="store_true",
                     help="instead of throughput: open-loop replay of synthetic recorded traces")
     ap.add_argument("--rp-batch", type=int, default=0,
@@ -144,6 +147,10 @@ def main() -> int:
     if args.replay:
         res = replay_study(w, steps=args.steps or 2048, batch=args.rp_batch or w.batch,
                            block=args.block, memory=args.rp_memory, device=dev)
+        print(json.dumps(res), flush=True)
+        return 0
+    if args.entry_points:
+        res = entry_point_rates(w, steps=args.steps or 10, warmup=args.warmup, device=dev)
         print(json.dumps(res), flush=True)
         return 0
     if args.state_error:
@@ -915,6 +922,58 @@ PROFILE_COMMANDS = {
     "replay_trace_summary": "python3 $R/bench.py --summarize-trace $OUT/prof_replay "
                             "k_replay.m1_long",
 }
+
+
+def entry_point_rates(w, steps, warmup, device):
+    """Rates of the boundary's other two calls on one layer's worth of entries: the
+    rounding step alone (fp32 values in, codes and group scales out) and the
+    threshold words alone (32-bit words out). Each is timed over `steps` launches
+    between two events on the launch stream; bytes are the call's own reads and
+    writes (fp32 in 4 B, codes, 4 B per scale, 4 B per threshold word)."""
+    import torch
+
+    import paper_2609_39185_amd as ssmq
+    from paper_2609_39185_amd import workloads as wl
+
+    n = w.entries_per_layer
+    head = w.headdim * w.dstate
+    stream = torch.cuda.current_stream(device)
+    g = torch.Generator(device=device).manual_seed(7)
+    h = torch.randn(n, generator=g, device=device) * 0.3
+    code_dtype = {"bf16": torch.int16, "fp16": torch.int16, "e4m3": torch.uint8,
+                  "int8": torch.uint8, "int4": torch.uint8}
+
+    def timed(fn):
+        for k in range(warmup):
+            fn(k)
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for k in range(steps):
+            fn(warmup + k)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) * 1e3 / steps
+
+    out = {"workload": w.name, "entries": n, "launches_timed": steps, "requantize": {}, "dither_fill": {}}
+    for fmt, rule, group in (("bf16", "rtn", 0), ("bf16", "weyl", 0), ("bf16", "sr", 0),
+                             ("bf16", "philox", 0), ("e4m3", "weyl", head), ("e4m3", "weyl", 128),
+                             ("int8", "weyl", 128), ("int4", "weyl", 128)):
+        codes = torch.empty(n // (2 if fmt == "int4" else 1), dtype=code_dtype[fmt], device=device)
+        scale = torch.empty(n // group, device=device) if fmt in ("e4m3", "int8", "int4") else None
+        us = timed(lambda k: ssmq.requantize(h, codes, scale, rule=rule, fmt=fmt, head_size=head,
+                                             dither_block=w.dither_block, scale_group=group,
+                                             step=k, stream=stream))
+        nbytes = n * 4 + int(n * state_bytes_per_entry(fmt)) + (4 * (n // group) if scale is not None else 0)
+        out["requantize"][f"{fmt}/{group}:{rule}" if scale is not None else f"{fmt}:{rule}"] = {
+            "us": us, "GBps": nbytes / (us * 1e3), "bytes": nbytes}
+        del codes, scale
+    words = torch.empty(n, dtype=torch.int32, device=device)
+    for rule in ("weyl", "sr", "philox"):
+        us = timed(lambda k: ssmq.dither_fill(words, rule=rule, step=k, dither_block=w.dither_block,
+                                              stream=stream))
+        out["dither_fill"][rule] = {"us": us, "GBps": 4 * n / (us * 1e3), "bytes": 4 * n}
+    return out
 
 
 def cpu_baseline(w, variant, target_s):

@@ -485,11 +485,32 @@ __global__ __launch_bounds__(256) void k_dither_fill(DitherArgs a) {
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   const int64_t e = q * 4;
   if (e >= a.n) return;
-  const int64_t lim = (a.n - e < 4) ? (a.n - e) : 4;
-  for (int64_t k = 0; k < lim; ++k) {
-    const uint64_t ge = a.entry_base + static_cast<uint64_t>(e + k);
-    a.out[e + k] = (R == kRTN) ? (1u << 23) : (entry_thr<R>(ge, a.thr) >> 8);
+  const uint64_t ge = a.entry_base + static_cast<uint64_t>(e);
+  if (a.n - e >= 4 && (reinterpret_cast<uintptr_t>(a.out) & 15u) == 0) {
+    // Four whole words to a 16-byte aligned address: one 16-byte store, and one
+    // Philox block when the four entries are the words of one block.
+    uint32_t w[4];
+    if constexpr (R == kPHILOX) {
+      if ((ge & 3u) == 0) {
+        const uint64_t blk = ge >> 2;
+        philox4x32_10(static_cast<uint32_t>(blk), static_cast<uint32_t>(blk >> 32), a.thr.step, 0u,
+                      a.thr.seed, a.thr.layer, w);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) w[k] >>= 8;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) w[k] = entry_thr<R>(ge + k, a.thr) >> 8;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) w[k] = (R == kRTN) ? (1u << 23) : (entry_thr<R>(ge + k, a.thr) >> 8);
+    }
+    store_stream(a.out + e, make_uint4(w[0], w[1], w[2], w[3]));
+    return;
   }
+  const int64_t lim = (a.n - e < 4) ? (a.n - e) : 4;
+  for (int64_t k = 0; k < lim; ++k)
+    a.out[e + k] = (R == kRTN) ? (1u << 23) : (entry_thr<R>(ge + static_cast<uint64_t>(k), a.thr) >> 8);
 }
 
 // ---------------------------------------------------------------------------

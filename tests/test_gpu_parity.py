@@ -46,6 +46,19 @@ def test_dither_fill_bit_exact(ssmq, rule, block, entry_base, n):
         assert out.cpu().numpy()[0] == -1
 
 
+@pytest.mark.parametrize("rule", ["sr", "weyl", "philox"])
+def test_dither_fill_unaligned_output(ssmq, rule):
+    """An output 4-byte but not 16-byte aligned takes the word-by-word path."""
+    n, base = 5003, 12
+    say(f"case dither_fill {rule} output offset 4 bytes, n {n}")
+    buf = torch.full((n + 1,), -1, dtype=torch.int32, device=DEV)
+    ssmq.dither_fill(buf[1:], rule=rule, seed=2, layer=4, step=99, entry_base=base, dither_block=16)
+    torch.cuda.synchronize()
+    got = buf.cpu().numpy().view(np.uint32)
+    assert got[0] == 0xFFFFFFFF
+    assert np.array_equal(got[1:], oracle.thresholds(rule, 2, 4, 99, base, n, 16))
+
+
 # --------------------------------------------------------------------------
 # requantize: bit-exact on identical fp32 inputs, edge suites included
 # --------------------------------------------------------------------------
