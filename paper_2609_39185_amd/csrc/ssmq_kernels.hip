@@ -480,6 +480,44 @@ __global__ __launch_bounds__(256) void k_requant_scaled(RequantArgs a) {
   }
 }
 
+// Groups of 256 * 16 * CPT entries (4096 or 8192, e.g. one scale per 64x128
+// head): one workgroup per group, its values held in registers between the
+// maximum and the rounding, so the fp32 input is read once.
+template <int F, int R, int CPT>
+__global__ __launch_bounds__(256) void k_requant_group_wg(RequantArgs a) {
+  const int t = threadIdx.x;
+  const int64_t e0 = static_cast<int64_t>(blockIdx.x) * a.group;
+  float h[CPT][16];
+  float m = 0.0f;
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    load_floats<16>(a.h + e0 + (static_cast<int64_t>(j) * 256 + t) * 16, h[j]);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) m = fmaxf(m, __builtin_fabsf(h[j][k]));
+  }
+  __shared__ uint32_t red[4];
+  __shared__ float rsh;
+  const uint32_t mw = lane_umax(__float_as_uint(m), 64);
+  if ((t & 63) == 0) red[t >> 6] = mw;
+  __syncthreads();
+  if (t == 0) {
+    const uint32_t w = max(max(red[0], red[1]), max(red[2], red[3]));
+    const float sc = group_scale<F>(__uint_as_float(w));
+    a.scale[blockIdx.x] = sc;
+    rsh = recip_scale(sc);
+  }
+  __syncthreads();
+  const float rs = rsh;
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    const int64_t e = e0 + (static_cast<int64_t>(j) * 256 + t) * 16;
+    const uint64_t ge = a.entry_base + static_cast<uint64_t>(e);
+    const chunk_t<F> out = quantize_any<F, R>(
+        h[j], rs, chunk_thr<R, 16>(ge, a.thr, thr_base<R>(ge, a.thr), a.toff), chunk_has_nan<16>(h[j]));
+    *reinterpret_cast<chunk_t<F>*>(static_cast<uint8_t*>(a.codes) + chunk_bytes_at<F>(e)) = out;
+  }
+}
+
 template <int R>
 __global__ __launch_bounds__(256) void k_dither_fill(DitherArgs a) {
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -765,9 +803,25 @@ static hipError_t launch_requant_f(const RequantArgs& a, int rule, hipStream_t s
   return hipGetLastError();
 }
 
+template <int F, int CPT>
+static hipError_t launch_requant_group_wg(const RequantArgs& a, int rule, hipStream_t s) {
+  const unsigned grid = static_cast<unsigned>(a.n / a.group);
+  switch (rule) {
+    case kRTN: hipLaunchKernelGGL((k_requant_group_wg<F, kRTN, CPT>), dim3(grid), dim3(256), 0, s, a); break;
+    case kSR: hipLaunchKernelGGL((k_requant_group_wg<F, kSR, CPT>), dim3(grid), dim3(256), 0, s, a); break;
+    case kPHILOX: hipLaunchKernelGGL((k_requant_group_wg<F, kPHILOX, CPT>), dim3(grid), dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((k_requant_group_wg<F, kWEYL, CPT>), dim3(grid), dim3(256), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
 template <int F>
 static hipError_t launch_requant_scaled(const RequantArgs& a, int rule, hipStream_t s) {
   const int64_t n_groups = a.n / a.group;
+  if (n_groups <= 0x7FFFFFFFLL) {
+    if (a.group == 4096) return launch_requant_group_wg<F, 1>(a, rule, s);
+    if (a.group == 8192) return launch_requant_group_wg<F, 2>(a, rule, s);
+  }
   const int64_t gpw = 64 / a.lanes_per_group;
   int64_t blocks = (n_groups + 4 * gpw - 1) / (4 * gpw);
   if (blocks > 65536) blocks = 65536;

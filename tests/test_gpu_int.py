@@ -47,7 +47,7 @@ def _edge_blocks(fmt, group, n_groups, rng):
 
 @pytest.mark.parametrize("fmt", ["int8", "int4"])
 @pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
-@pytest.mark.parametrize("group,n_groups", [(16, 700), (128, 300), (8192, 9), (48, 33)])
+@pytest.mark.parametrize("group,n_groups", [(16, 700), (128, 300), (8192, 9), (48, 33), (4096, 6)])
 def test_requantize_int_bit_exact(ssmq, fmt, rule, group, n_groups):
     say(f"case requantize {fmt} {rule} group {group} x {n_groups}")
     x = _edge_blocks(fmt, group, n_groups, np.random.default_rng(group + QMAX[fmt]))

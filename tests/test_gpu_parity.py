@@ -116,7 +116,7 @@ def test_requantize_bit_exact(ssmq, fmt, rule, n, entry_base, block):
 
 @pytest.mark.parametrize("rule", ["rtn", "sr", "weyl", "philox"])
 @pytest.mark.parametrize("group,n_groups", [(16, 700), (128, 300), (8192, 9), (48, 33),
-                                            (2048, 5)])
+                                            (2048, 5), (4096, 6)])
 def test_requantize_e4m3_bit_exact(ssmq, rule, group, n_groups):
     say(f"case requantize e4m3 {rule} group {group} x {n_groups}")
     rng = np.random.default_rng(group)
