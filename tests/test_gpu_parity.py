@@ -165,6 +165,15 @@ def test_step_head_tile_philox(ssmq, fmt, q):
     check_step(fmt, "philox", *M2_SMALL, seed=12, what="philox head tile", step=7, layer=3, **q)
 
 
+@pytest.mark.parametrize("fmt,q", [("bf16", {"dither_block": 8192}), ("bf16", {"dither_block": 1 << 20}),
+                                   ("e4m3", {"dither_block": 4096}), ("e4m3", {"scale_group": 128, "dither_block": 4096}),
+                                   ("int8", {"scale_group": 128, "dither_block": 8192})])
+def test_step_dither_block_wider_than_a_pass(ssmq, fmt, q):
+    """Weyl blocks longer than one pass of a workgroup: the chunks' threshold bases
+    are computed directly rather than stepped from the first."""
+    check_step(fmt, "weyl", *M2_SMALL, seed=14, what="wide dither block", step=21, layer=6, **q)
+
+
 def test_step_philox_mamba1_rows(ssmq):
     check_step("fp16", "philox", "mamba1", 3, 200, 1, 16, 1, seed=13, what="philox rows",
                step=11, layer=2)
