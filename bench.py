@@ -76,6 +76,8 @@ def parse_args():
     ap.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                     help="turn rocprofv3 CSV output (kernel trace with --stats, then --pmc "
                          "FETCH_SIZE, then --pmc WRITE_SIZE) into the summaries under profiles/")
+    ap.add_argument("--summarize-entry-trace", metavar="TRACE_DIR",
+                    help="write the entry-point kernel trace summary under profiles/")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_DIR", "NAME"),
                     help="turn a rocprofv3 --kernel-trace --stats run of --replay into "
                          "profiles/NAME.kernel_trace.md")
@@ -127,6 +129,8 @@ def main() -> int:
         return summarize_valu(args.workload, args.summarize_valu)
     if args.summarize_trace:
         return summarize_replay_trace(*args.summarize_trace)
+    if args.summarize_entry_trace:
+        return summarize_entry_points_trace(args.summarize_entry_trace)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this benchmark measures one GPU only; the state update shards "
@@ -863,6 +867,33 @@ def summarize_replay_trace(trace_dir: str, name: str) -> int:
     return 0
 
 
+def summarize_entry_points_trace(trace_dir: str) -> int:
+    """Write profiles/entry_points.hybrid_m2_stack.kernel_trace.md from a kernel
+    trace of `bench.py --entry-points` (PROFILE_COMMANDS["entry_trace"]): per
+    requantize and threshold-fill kernel instance, calls and durations."""
+    import re
+
+    stats = _csv_rows(trace_dir, "kernel_stats.csv")
+    lines = ["# Kernel trace of the requantize and threshold-fill calls (268,435,456 entries per launch)", "",
+             "Command (repository root as $R, an output directory as $OUT, run from /tmp with TMPDIR=/tmp):", "",
+             f"    {PROFILE_COMMANDS['entry_trace']}",
+             f"    {PROFILE_COMMANDS['entry_trace_summary']}", "",
+             "Template arguments: format code (0 fp16, 1 bf16, 2 E4M3, 4 INT8, 5 INT4), rule code "
+             "(0 RTN, 1 hash SR, 2 Weyl, 3 Philox), and for the per-group kernel the chunks per thread.", "",
+             "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: r["Name"]):
+        if not re.search(r"k_requant|k_dither_fill", r["Name"]):
+            continue
+        lines.append(f"| `{_short_kernel(r['Name'])}` "
+                     f"| {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | {float(r['MinNs']) / 1e3:.1f} | "
+                     f"{float(r['MaxNs']) / 1e3:.1f} |")
+    os.makedirs(PROFILE_DIR, exist_ok=True)
+    with open(os.path.join(PROFILE_DIR, "entry_points.hybrid_m2_stack.kernel_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 def summarize_valu(workload: str, pmc_dir: str) -> int:
     """Write profiles/k_update_slab.<workload>.valu.md: per variant, VALU
     instructions per wave and per entry (lane operations), and the VALU busy
@@ -919,6 +950,9 @@ PROFILE_COMMANDS = {
     "valu_summary": "python3 $R/bench.py --summarize-valu $OUT/pmc_busy",
     "replay_trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/prof_replay "
                     "-o run -- python3 $R/bench.py --replay --steps 4096",
+    "entry_trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/prof_entry "
+                   "-o run -- python3 $R/bench.py --entry-points",
+    "entry_trace_summary": "python3 $R/bench.py --summarize-entry-trace $OUT/prof_entry",
     "replay_trace_summary": "python3 $R/bench.py --summarize-trace $OUT/prof_replay "
                             "k_replay.m1_long",
 }
