@@ -1065,6 +1065,14 @@ def cpu_baseline(w, variant, target_s):
     with ThreadPoolExecutor(max_workers=cores) as pool:
         calls = sum(pool.map(worker, [t0 + target_s] * cores))
     wall = time.perf_counter() - t0
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
+    host = {"cpu_model": model, "cpu_count": os.cpu_count(),
+            "usable_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
     return {
         "value": calls * tile_bytes / wall / 1e9,
         "unit": "GB/s",
@@ -1074,6 +1082,7 @@ def cpu_baseline(w, variant, target_s):
                   f"({P}x{N} per head) of one layer of {w.name}, {fmt} {rule}, the C oracle, "
                   f"{wall:.1f} s wall",
         "single_thread": single,
+        "host": host,
     }
 
 
