@@ -89,8 +89,12 @@ def oracle_update(fmt, rule, codes, scale, x, dt, A, B, C, D, **q):
                                None if D is None else D.numpy(), **kw)
 
 
-def check_step(fmt, rule, family, batch, nheads, headdim, dstate, ngroups, seed, what="", **q):
-    """One fused step on seeded inputs: GPU vs oracle at the stated bar."""
+def check_step(fmt, rule, family, batch, nheads, headdim, dstate, ngroups, seed, what="",
+               dither_seed=None, **q):
+    """One fused step on seeded inputs: GPU vs oracle at the stated bar. seed draws
+    the inputs; dither_seed, when given, is the rounding's seed (sigma)."""
+    if dither_seed is not None:
+        q["seed"] = dither_seed
     A, D = wl.layer_params(family, nheads, dstate, seed)
     x, dt, B, C = wl.step_inputs(batch, nheads, headdim, dstate, ngroups, seed + 1)
     codes, scale = wl.initial_state(fmt, batch, nheads, headdim, dstate, seed + 2,
