@@ -11,7 +11,16 @@ headline variant (bf16 state, Weyl dither); the other formats and rules are
 reported under "variants". Each variant's timed region is exactly --steps steps
 between two events on the launch stream; since that stream carries only the
 update launches, the region's time over their number is the average launch
-duration behind roofline.achieved.
+duration behind roofline.achieved. With --rounds R the variants are timed in R
+interleaved rounds and each reports its median round; --graph replays the timed
+steps from one HIP graph. cpu_baseline times the CPU oracle on one thread and on
+every usable core (at most 16).
+
+Other modes print their own JSON line instead: --entry-points (ssmq_requantize
+and ssmq_dither_fill alone), --state-error (quantized states against an FP32
+twin in lockstep), --replay (open-loop replay of synthetic recorded traces); the
+--summarize-* options turn rocprofv3 CSV output into the summaries under
+profiles/.
 """
 from __future__ import annotations
 
