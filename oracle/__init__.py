@@ -65,7 +65,32 @@ def lib() -> ctypes.CDLL:
         return _lib
     if not os.path.exists(build_oracle.LIBRARY):
         build_oracle.build()
-    L = ctypes.CDLL(build_oracle.LIBRARY)
+    _lib = load_library(build_oracle.LIBRARY)
+    return _lib
+
+
+class using_library:
+    """Context manager: route this module's functions through another build of the
+    oracle (the mutation tests load copies with a planted mistake)."""
+
+    def __init__(self, path: str):
+        self.path = path
+
+    def __enter__(self):
+        global _lib
+        self.saved = _lib
+        _lib = load_library(self.path)
+        return _lib
+
+    def __exit__(self, *exc):
+        global _lib
+        _lib = self.saved
+        return False
+
+
+def load_library(path: str) -> ctypes.CDLL:
+    """Open an oracle library at `path` and declare its functions' signatures."""
+    L = ctypes.CDLL(path)
     L.orc_weyl_constants.argtypes = [ctypes.POINTER(_u32)]
     L.orc_weyl_constants.restype = None
     L.orc_fmix32.argtypes = [_u32]
@@ -106,7 +131,6 @@ def lib() -> ctypes.CDLL:
     L.orc_replay.argtypes = [_int, _int, _u32, _u32, _u32, _u64, _u64, _i64, _i64, _i64, _i64,
                              _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.orc_replay.restype = _int
-    _lib = L
     return L
 
 

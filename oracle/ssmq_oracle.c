@@ -23,9 +23,12 @@
  *   dA     = fl32(exp(z))                    (exp in double, then one rounding)
  *   dx     = fl32(dt * x_p)
  *   w      = fl32(dx * B_n)
- *   h_new  = fma(dA, h_prev, w)              (one rounding), h_prev = decode(code)
- *            E4M3 and INT8/INT4: the stored value is v * s_old (v the exact code
- *            value), and dA * (v * s_old) is taken as fma(fl32(dA * s_old), v, w)
+ *   h_prev = decode(code)                    fp16 / bf16 / fp32: the code's value
+ *          = fl32(v * s_old)                 E4M3, INT8, INT4: the code's value v
+ *                                            times its group's old scale, in fp32
+ *                                            (every format is simulated in FP32,
+ *                                            Appendix B "Formats")
+ *   h_new  = fma(dA, h_prev, w)              (one rounding)
  *   y_p    = sum_n C_n h_new + D x_p         (accumulated in double)
  * then h_new is written back under the chosen rounding rule.
  */
@@ -639,14 +642,10 @@ int orc_state_update_ex(int f, int rule, uint32_t seed, uint32_t layer, uint32_t
                     const float z = dtv * a;
                     const float dA = (float)exp((double)z);
                     const float v = code_value(f, load_code(f, state, k));
+                    /* the stored value: scaled formats multiply by the old scale */
+                    const float h_prev = is_scaled(f) ? v * scale[k / group] : v;
                     const float w = dx * Bg[n];
-                    float h_new;
-                    if (is_scaled(f)) {
-                        const float dAs = dA * scale[k / group]; /* decay times old scale */
-                        h_new = fmaf(dAs, v, w);
-                    } else {
-                        h_new = fmaf(dA, v, w);
-                    }
+                    const float h_new = fmaf(dA, h_prev, w);
                     hn[k] = h_new;
                     acc += (double)Cg[n] * (double)h_new;
                 }

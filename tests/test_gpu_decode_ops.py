@@ -9,7 +9,7 @@ import torch
 import oracle
 from paper_2609_39185_amd import workloads as wl
 
-from ._parity import DEV, assert_codes, say
+from ._parity import DEV, Bar, say
 
 pytestmark = pytest.mark.gpu
 
@@ -58,15 +58,14 @@ def test_step_with_dt_bias_softplus_and_gate(ssmq, fmt, rule, family, shape, q, 
         block=q.get("dither_block", 16), group=q.get("scale_group", 0),
         dt_bias=None if dt_bias is None else dt_bias.numpy(), dt_softplus=softplus,
         z=None if z is None else z.numpy())
-    assert_codes(fmt, wl.to_numpy_codes(fmt, st.cpu()), r_codes, "decode ops")
+    bar = Bar(fmt, "decode ops").codes(wl.to_numpy_codes(fmt, st.cpu()), r_codes)
     if sc is not None:
-        np.testing.assert_array_equal(sc.cpu().numpy(), r_scale)
+        bar.scales(sc.cpu().numpy(), r_scale)
     Ch = np.repeat(C.numpy().astype(np.float64), h // g, axis=1)[:, :, None, :]
     mag = np.abs(Ch * r_h.astype(np.float64)).sum(-1) + np.abs(D.numpy()[None, :, None] * x.numpy())
     if z is not None:
         mag = mag * np.abs(torch.nn.functional.silu(z.double()).numpy())
-    err = np.abs(y.cpu().numpy().astype(np.float64) - r_y)
-    assert np.all(err <= 1e-5 * (mag + np.abs(r_y)) + 1e-30), err.max()
+    bar.y(y.cpu().numpy(), r_y, mag).check()
 
 
 @pytest.mark.parametrize("batch,channels,width", [(1, 7, 4), (3, 1536, 4), (2, 8192 + 2 * 8 * 128, 4),
@@ -141,11 +140,10 @@ def test_composed_mamba2_decode_step(ssmq, fmt, rule, group):
         fmt, rule, wl.to_numpy_codes(fmt, codes), None if scale is None else scale.numpy(), xs,
         dt_raw, A.numpy(), Bs, Cs, D.numpy(), step=9, layer=1, block=128, group=group,
         dt_bias=dt_bias, dt_softplus=True, z=z)
-    assert_codes(fmt, wl.to_numpy_codes(fmt, st.cpu()), r_codes, "composed step")
+    bar = Bar(fmt, "composed step").codes(wl.to_numpy_codes(fmt, st.cpu()), r_codes)
     if sc is not None:
-        np.testing.assert_array_equal(sc.cpu().numpy(), r_scale)
+        bar.scales(sc.cpu().numpy(), r_scale)
     Ch = np.repeat(Cs.astype(np.float64), H // G, axis=1)[:, :, None, :]
     mag = (np.abs(Ch * r_h.astype(np.float64)).sum(-1) + np.abs(D.numpy()[None, :, None] * xs))
     mag = mag * np.abs(torch.nn.functional.silu(torch.from_numpy(z).double()).numpy())
-    err = np.abs(y.cpu().numpy().astype(np.float64) - r_y)
-    assert np.all(err <= 1e-5 * (mag + np.abs(r_y)) + 1e-30), err.max()
+    bar.y(y.cpu().numpy(), r_y, mag).check()

@@ -129,7 +129,7 @@ def test_int_dithers_are_unbiased(orc, rule):
 
 @pytest.mark.parametrize("fmt", ["int8", "int4"])
 def test_int_step_is_the_recurrence_with_block_scale(orc, fmt):
-    """h_new = fma(fl32(dA s_old), k, w) against a float64 evaluation of eq. (rec);
+    """h_new = fma(dA, fl32(k s_old), w) against a float64 evaluation of eq. (rec);
     y from the pre-rounding state; the new scale is max|h_new| / qmax per block."""
     batch, nheads, headdim, dstate, ngroups, group = 2, 4, 8, 32, 2, 16
     A, D = wl.layer_params("mamba2", nheads, dstate, 7)

@@ -1,0 +1,195 @@
+"""Pins of the oracle's fused step on the scaled formats (E4M3, INT8, INT4; CPU only).
+
+The stored value of a scaled format is its code's value times the group's fp32
+scale (Appendix B "Formats"). The step must therefore be eq. (rec) of Section 2
+applied to the values dequantized with the OLD scales, and the new scale must be
+max|h_new| / qmax of the new values (Section 2 "Low-precision storage"). The
+reference here decodes the codes from the format definitions independently of
+the oracle (torch's float8_e4m3fn for E4M3, two's complement bytes and nibbles
+for INT8 / INT4) and evaluates the recurrence in float64.
+
+The mutation tests build copies of the oracle with one mistake planted in the
+step (the old scale dropped, a neighbouring group's scale read, the decay and the
+old scale multiplied first) and check that the pins reject each of them.
+"""
+import os
+import subprocess
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import build_oracle
+from paper_2609_39185_amd import workloads as wl
+
+QMAX = {"e4m3": 448.0, "int8": 127.0, "int4": 7.0}
+SHAPES = {  # (family, batch, nheads, headdim, dstate, ngroups)
+    "mamba2": ("mamba2", 2, 4, 8, 32, 2),
+    "mamba1": ("mamba1", 2, 12, 1, 16, 1),
+}
+
+
+def _code_values(fmt, codes):
+    """Exact value of every entry's code (no scale) from the format definition."""
+    c = np.ascontiguousarray(codes, np.uint8).ravel()
+    if fmt == "e4m3":
+        return torch.from_numpy(c.copy()).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    if fmt == "int8":
+        return c.view(np.int8).astype(np.float64)
+    lo = (c & 0xF).astype(np.int64)
+    hi = (c >> 4).astype(np.int64)
+    v = np.empty(2 * c.size, np.int64)
+    v[0::2], v[1::2] = lo, hi
+    return (((v ^ 8) - 8)).astype(np.float64)  # 4-bit two's complement
+
+
+def _case(fmt, shape, group, seed):
+    family, batch, nheads, headdim, dstate, ngroups = shape
+    A, D = wl.layer_params(family, nheads, dstate, seed)
+    x, dt, B, C = wl.step_inputs(batch, nheads, headdim, dstate, ngroups, seed + 1)
+    p = {k: v.numpy() for k, v in dict(A=A, D=D, x=x, dt=dt, B=B, C=C).items()}
+    rng = np.random.default_rng(seed + 2)
+    n = batch * nheads * headdim * dstate
+    g = group or headdim * dstate
+    # every group gets its own magnitude, so that scales differ from group to group
+    mag = np.exp(rng.uniform(-9, 2, n // g))
+    h0 = (rng.standard_normal(n) * np.repeat(mag, g)).astype(np.float32)
+    codes0, s0 = oracle.requantize(fmt, "rtn", h0, group=g, block=16)
+    per = 2 if fmt == "int4" else 1
+    codes0 = codes0.reshape(batch, nheads, headdim, dstate // per)
+    return p, codes0, s0, g
+
+
+def _reference(fmt, shape, p, codes0, s0, g):
+    """float64 eq. (rec) from the values stored before the step (old scales)."""
+    family, batch, nheads, headdim, dstate, ngroups = shape
+    prev = (_code_values(fmt, codes0) * np.repeat(s0.astype(np.float64), g)).reshape(
+        batch, nheads, headdim, dstate)
+    hpg = nheads // ngroups
+    Bh = np.repeat(p["B"].astype(np.float64), hpg, axis=1)
+    Ch = np.repeat(p["C"].astype(np.float64), hpg, axis=1)
+    dtv = p["dt"].astype(np.float64)
+    A = p["A"].astype(np.float64)
+    if family == "mamba1":
+        dA = np.exp(dtv[:, :, None, None] * A[None, :, None, :])
+    else:
+        dA = np.exp(dtv * A[None, :])[:, :, None, None]
+    w = (dtv[:, :, None] * p["x"].astype(np.float64))[..., None] * Bh[:, :, None, :]
+    return dA * prev, w, Ch
+
+
+def _pin_failures(fmt, shape, group, seed=7, rule="weyl"):
+    """Run the oracle's step on one case; return the list of pins it fails."""
+    p, codes0, s0, g = _case(fmt, shape, group, seed)
+    new, s1, y, hnew = oracle.state_update(fmt, rule, codes0, s0, p["x"], p["dt"], p["A"],
+                                           p["B"], p["C"], p["D"], group=group, block=16)
+    decay_term, w, Ch = _reference(fmt, shape, p, codes0, s0, g)
+    ref = decay_term + w
+    failed = []
+    # fl32 of the stored value, of dA, of dt x and of w, and the final rounding:
+    # at most about 4 units of 2^-24 relative to |dA h_prev| + |w|
+    tol = 4e-7 * (np.abs(decay_term) + np.abs(w)) + 1e-38
+    if not np.all(np.abs(hnew.astype(np.float64) - ref) <= tol):
+        failed.append("h_new is not eq. (rec) of the old stored values")
+    yref = ((Ch[:, :, None, :] * hnew.astype(np.float64)).sum(-1)
+            + p["D"].astype(np.float64)[None, :, None] * p["x"].astype(np.float64))
+    if not np.allclose(y, yref, rtol=1e-12, atol=1e-30):
+        failed.append("y is not C h_new + D x")
+    m = np.abs(hnew.reshape(-1, g)).max(axis=1)
+    want_s = (m / np.float32(QMAX[fmt])).astype(np.float32)  # IEEE division, rounded once
+    want_s[want_s < np.finfo(np.float32).tiny] = 0.0
+    if not np.array_equal(s1, want_s):
+        failed.append("new scale is not max|h_new| / qmax")
+    return failed
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "int8", "int4"])
+@pytest.mark.parametrize("shape", ["mamba2", "mamba1"])
+@pytest.mark.parametrize("group", [16, 0])
+def test_scaled_step_is_the_recurrence_of_the_stored_values(fmt, shape, group):
+    """h_new against a float64 eq. (rec) from the values dequantized with the old
+    scales (per 16-entry group and one scale per head), y = C h_new + D x, and the
+    new scale max|h_new| / qmax."""
+    assert _pin_failures(fmt, SHAPES[shape], group) == []
+
+
+def _rne32(q: Fraction) -> np.float32:
+    """The fp32 value nearest to the rational q (ties to even), by exact comparison."""
+    f = np.float32(float(q))
+    cands = [np.nextafter(f, np.float32(-np.inf)), f, np.nextafter(f, np.float32(np.inf))]
+    best = min(cands, key=lambda c: (abs(Fraction(float(c)) - q),
+                                     int(np.array(c, np.float32).view(np.uint32)) & 1))
+    return np.float32(best)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "int8", "int4"])
+def test_scaled_step_rounds_in_the_stated_order(fmt):
+    """The oracle's fp32 order, checked exactly on a sample of entries with rational
+    arithmetic: h_prev = fl32(v s_old), then h_new = fl32(dA h_prev + w) rounded
+    once (the fma), with dA = fl32(exp(fl32(dt A))) and w = fl32(fl32(dt x) B)."""
+    shape = SHAPES["mamba2"]
+    family, batch, nheads, headdim, dstate, ngroups = shape
+    p, codes0, s0, g = _case(fmt, shape, 16, 3)
+    _, _, _, hnew = oracle.state_update(fmt, "rtn", codes0, s0, p["x"], p["dt"], p["A"], p["B"],
+                                        p["C"], p["D"], group=16, block=16)
+    v = _code_values(fmt, codes0).reshape(batch, nheads, headdim, dstate)
+    hpg = nheads // ngroups
+    f32 = np.float32
+    rng = np.random.default_rng(0)
+    for k in rng.choice(hnew.size, 600, replace=False):
+        b, hh, pp, nn = np.unravel_index(k, hnew.shape)
+        dtv = f32(p["dt"][b, hh])
+        dA = f32(np.exp(np.float64(f32(dtv * p["A"][hh]))))
+        s_old = f32(s0[k // 16])
+        h_prev = _rne32(Fraction(float(v[b, hh, pp, nn])) * Fraction(float(s_old)))
+        w = f32(f32(dtv * p["x"][b, hh, pp]) * p["B"][b, hh // hpg, nn])
+        want = _rne32(Fraction(float(dA)) * Fraction(float(h_prev)) + Fraction(float(w)))
+        assert hnew[b, hh, pp, nn] == want, (k, hnew[b, hh, pp, nn], want)
+
+
+# --------------------------------------------------------------------------
+# mutation tests: a mistake planted in a copy of the oracle must fail a pin
+# --------------------------------------------------------------------------
+STEP_LINE = "const float h_prev = is_scaled(f) ? v * scale[k / group] : v;"
+FMA_LINE = "const float h_new = fmaf(dA, h_prev, w);"
+MUTANTS = {
+    "old scale dropped": [(STEP_LINE, "const float h_prev = v;")],
+    "neighbouring group's scale": [
+        (STEP_LINE, "const float h_prev = is_scaled(f) ? v * scale[(k / group) ^ 1] : v;")],
+    "decay times old scale first": [
+        (STEP_LINE, "const float h_prev = v;"),
+        (FMA_LINE, "const float h_new = is_scaled(f) ? fmaf(dA * scale[k / group], h_prev, w)"
+                   " : fmaf(dA, h_prev, w);")],
+}
+
+
+def _build_mutant(tmp_path, edits):
+    src = open(build_oracle.SOURCE).read()
+    for old, new in edits:
+        assert src.count(old) == 1, old
+        src = src.replace(old, new)
+    c = os.path.join(tmp_path, "mutant.c")
+    so = os.path.join(tmp_path, "libmutant.so")
+    with open(c, "w") as fh:
+        fh.write(src)
+    subprocess.run(["gcc", *build_oracle.CFLAGS, "-o", so, c, "-lm"], check=True)
+    return so
+
+
+@pytest.mark.parametrize("mutant", sorted(MUTANTS))
+def test_pins_reject_planted_mistakes(tmp_path, mutant):
+    so = _build_mutant(str(tmp_path), MUTANTS[mutant])
+    with oracle.using_library(so):
+        if mutant == "decay times old scale first":
+            # both orders are eq. (rec) within a few fp32 roundings: the float64
+            # pin accepts it, and only the exact order check tells them apart
+            assert _pin_failures("e4m3", SHAPES["mamba2"], 16) == []
+            with pytest.raises(AssertionError):
+                test_scaled_step_rounds_in_the_stated_order("e4m3")
+        else:
+            for fmt in ("e4m3", "int8", "int4"):
+                for group in (16, 0):
+                    assert "h_new is not eq. (rec) of the old stored values" in _pin_failures(
+                        fmt, SHAPES["mamba2"], group), (fmt, group)
