@@ -80,6 +80,11 @@ def parse_args():
                     help="timed regions per variant, interleaved across variants; the median is reported")
     ap.add_argument("--graph", action="store_true",
                     help="replay the timed steps from one HIP graph (removes host launch gaps)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads (HIP-graph timing, oracle timing, config-3 "
+                         "state error) in the default line")
+    ap.add_argument("--config-steps", type=int, default=20,
+                    help="timed steps per rule for each of the other workloads")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the streaming-kernel bandwidth ceiling")
     ap.add_argument("--summarize-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
@@ -307,6 +312,14 @@ def main() -> int:
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(w, variants[0], args.cpu_seconds)
 
+    # ---- the other workloads: device time per launch, oracle time, state error ------
+    configs = None
+    if not args.no_configs:
+        del layers
+        torch.cuda.empty_cache()
+        configs = config_sweep(dev, steps=args.config_steps, warmup=args.warmup,
+                               cpu_seconds=min(args.cpu_seconds, 2.0))
+
     head_var = variants[0]
     head_fmt, head_rule = head_var["fmt"], head_var["rule"]
     head = results[head_var["key"]]
@@ -351,6 +364,7 @@ def main() -> int:
         "cpu_baseline": cpu,
         "stream_ceiling": ceiling,
         "variants": results,
+        "configs": configs,
     }
     print(json.dumps(line), flush=True)
     return 0
@@ -681,6 +695,139 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
         "ms_per_step": 1e3 * elapsed / steps,
         "launches_per_step": L * (1 + len(runs)),
     }
+
+
+SWEEP_WORKLOADS = ("m1_small", "m2_ssd_b8", "m2_b64_fp8", "m1_long")
+
+
+def graph_launch_us(w, fmt, rule, group, L, steps, warmup, device, t0=1):
+    """Average device time per ssmq_state_update launch on workload w: all layers
+    resident, `steps` steps (each with its own step t) captured into one HIP graph
+    and replayed between two events on the launch stream. Returns (us per launch,
+    ms per step)."""
+    import torch
+
+    import paper_2609_39185_amd as ssmq
+    from paper_2609_39185_amd import workloads as wl
+
+    b, H, P, N, G = w.batch, w.nheads, w.headdim, w.dstate, w.ngroups
+    layers = []
+    for ell in range(L):
+        A, D = wl.layer_params(w.family, H, N, seed=1000 + ell, device=device)
+        x, dt, B, C = wl.step_inputs(b, H, P, N, G, seed=2000 + ell, device=device)
+        st, sc = wl.initial_state(fmt, b, H, P, N, seed=3000 + ell, group=group, device=device)
+        layers.append((st, sc, x, dt, A, B, C, D, torch.empty((b, H, P), device=device)))
+    stream = torch.cuda.current_stream(device)
+
+    def step(t, on):
+        for ell, (st, sc, x, dt, A, B, C, D, y) in enumerate(layers):
+            ssmq.state_update(st, sc, x, dt, A, B, C, D, y, rule=rule, fmt=fmt,
+                              dither_block=w.dither_block, scale_group=group, layer=ell, step=t,
+                              stream=on)
+
+    for k in range(warmup):
+        step(t0 + k, stream)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cap = torch.cuda.current_stream(device)
+        for k in range(steps):
+            step(t0 + warmup + k, cap)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    del graph, layers
+    torch.cuda.empty_cache()
+    return 1e3 * ms / (steps * L), ms / steps
+
+
+def oracle_layer_rate(w, fmt, rule, group, target_s, threads):
+    """The C oracle on a slice of one layer of workload w (Mamba-2: the heads of one
+    B/C group of one sequence; Mamba-1: one sequence's channels), repeated for about
+    target_s seconds on `threads` threads; returns (entries per second, sample text)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import oracle
+    from paper_2609_39185_amd import workloads as wl
+
+    H, P, N, G = w.nheads, w.headdim, w.dstate, w.ngroups
+    nh = H // G if w.family == "mamba2" else H
+    A, D = wl.layer_params(w.family, H, N, seed=1000)
+    x, dt, B, C = wl.step_inputs(1, H, P, N, G, seed=2000)
+    codes, scale = wl.initial_state(fmt, 1, H, P, N, seed=3000, group=group)
+    c = wl.to_numpy_codes(fmt, codes)[:, :nh]
+    per_head = P * N // (group or P * N) if scale is not None else 0
+    sc = None if scale is None else scale.numpy()[:nh * per_head]
+    args = (x.numpy()[:, :nh], dt.numpy()[:, :nh], A.numpy()[:nh], B.numpy()[:, :1],
+            C.numpy()[:, :1], D.numpy()[:nh])
+
+    def run():
+        oracle.state_update(fmt, rule, c, sc, *args, block=w.dither_block, group=group, step=1)
+
+    run()
+    def worker(deadline):
+        n = 0
+        while time.perf_counter() < deadline:
+            run()
+            n += 1
+        return n
+
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=threads) as pool:
+        calls = sum(pool.map(worker, [t0 + target_s] * threads))
+    wall = time.perf_counter() - t0
+    sample_entries = nh * P * N
+    return calls * sample_entries / wall, f"{calls} calls of {sample_entries} entries, {wall:.1f} s"
+
+
+def config_sweep(device, *, steps: int, warmup: int, cpu_seconds: float) -> dict:
+    """The measurement plan's other workloads, each in its own storage format and
+    under RTN, hash SR and Weyl: device time per launch (HIP graph, all layers
+    resident), the oracle's time for the same layer-step (extrapolated from a slice,
+    one thread and every usable core), and for the long-horizon Mamba-1 shape a short
+    state-error run against the FP32 twin (per rule, per block of steps)."""
+    from paper_2609_39185_amd import workloads as wl
+
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    cores = max(1, min(cores, int(os.environ.get("OMP_NUM_THREADS") or 16), 16))
+    out = {}
+    for name in SWEEP_WORKLOADS:
+        w = wl.WORKLOADS[name]
+        fmt = w.formats[0]
+        group = wl.scale_group_of(w, fmt)
+        L = w.layers
+        sbytes = state_bytes_per_launch(w, fmt, group)
+        entry = {"workload": w.name, "notes": w.notes, "format": fmt, "layers": L,
+                 "dither_block": w.dither_block, "entries_per_layer": w.entries_per_layer,
+                 "state_bytes_per_launch": sbytes, "launch": "hip_graph", "rules": {}}
+        for rule in ("rtn", "sr", "weyl"):
+            print(f"bench: {name} {fmt} {rule}: {steps} steps x {L} layers (HIP graph)",
+                  file=sys.stderr, flush=True)
+            us, ms_step = graph_launch_us(w, fmt, rule, group, L, steps, warmup, device)
+            r = {"us_per_launch": us, "ms_per_step": ms_step, "steps_per_s": 1e3 / ms_step,
+                 "state_GBps": sbytes / (us * 1e3), "pct_of_peak": 100.0 * sbytes / (us * 1e3) / PEAK_HBM_GBPS}
+            if cpu_seconds > 0:
+                e1, s1 = oracle_layer_rate(w, fmt, rule, group, cpu_seconds / 2, 1)
+                ea, sa = oracle_layer_rate(w, fmt, rule, group, cpu_seconds / 2, cores)
+                bpe = sbytes / w.entries_per_layer
+                r["oracle"] = {"us_per_layer_step_1_thread": 1e6 * w.entries_per_layer / e1,
+                               "us_per_layer_step_all_cores": 1e6 * w.entries_per_layer / ea,
+                               "GBps_1_thread": e1 * bpe / 1e9, "GBps_all_cores": ea * bpe / 1e9,
+                               "cores": cores, "sample_1_thread": s1, "sample_all_cores": sa}
+            entry["rules"][rule] = r
+        out[name] = entry
+    w = wl.WORKLOADS["m1_long"]
+    print("bench: m1_long state error against the FP32 twin, 512 steps x 64 layers",
+          file=sys.stderr, flush=True)
+    se = state_error_study(w, steps=512, layers=w.layers, block=128, device=device)
+    out["m1_long"]["state_error"] = {k: se[k] for k in ("metric", "steps", "block", "layers",
+                                                        "error", "error_over_sr_seed0",
+                                                        "tau_bin_share", "wall_s")}
+    return out
 
 
 def kernel_sources_digest() -> str:

@@ -1,5 +1,7 @@
-"""Build tests/c_abi_step, a C program that drives libssmq.so through
-include/ssmq.h and checks it against the oracle library (test infrastructure)."""
+"""Build the test programs (test infrastructure): tests/c_abi_step, a C program
+that drives libssmq.so through include/ssmq.h and checks it against the oracle
+library, and tests/scale_math_check, a HIP program that checks the group-scale
+division and reciprocal of the device code for every fp32 value in range."""
 from __future__ import annotations
 
 import os
@@ -10,6 +12,8 @@ ROOT = os.path.dirname(HERE)
 SOURCE = os.path.join(HERE, "c_abi_step.c")
 BINARY = os.path.join(HERE, "c_abi_step")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+SCALE_SOURCE = os.path.join(HERE, "scale_math_check.hip")
+SCALE_BINARY = os.path.join(HERE, "scale_math_check")
 
 
 def build(verbose: bool = False) -> str:
@@ -24,7 +28,24 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, BINARY)
+    build_scale_check(verbose)
     return BINARY
+
+
+def build_scale_check(verbose: bool = False) -> str:
+    """hipcc with the library's own floating-point flags (correctly rounded fp32
+    division, no contraction, denormals kept, no packed fp32)."""
+    tmp = SCALE_BINARY + ".tmp"
+    cmd = [os.path.join(ROCM, "bin", "hipcc"), "--offload-arch=gfx950", "-O3", "-std=c++17",
+           "-ffp-contract=off", "-fno-gpu-flush-denormals-to-zero",
+           "-fhip-fp32-correctly-rounded-divide-sqrt",
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-I", os.path.join(ROOT, "paper_2609_39185_amd", "csrc"), SCALE_SOURCE, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, SCALE_BINARY)
+    return SCALE_BINARY
 
 
 if __name__ == "__main__":

@@ -273,31 +273,93 @@ def test_small_mamba1_workload_64_steps(ssmq, rule):
     bar.check()
 
 
-def test_proposition1_through_the_kernel(ssmq):
-    """a = 1, constant write: e_T = -s(#{u_t < 1-f} - T(1-f)) on the GPU state."""
+def _prop1_prediction(rule, f, T, seed, layer, block, n):
+    """Proposition 1 (Section 3) for a = 1 and a constant write of f grid steps:
+    the accumulated error after T writes is -(N - T(1 - f)) steps, with N the
+    number of writes whose threshold u_t satisfies u_t < 1 - f (the writes that
+    round down). RTN is the rule with u = 1/2 (no ties occur here). Thresholds
+    come from the oracle's generator."""
+    count = np.zeros(n, np.int64)
+    for t in range(1, T + 1):
+        if rule == "rtn":
+            u = np.full(n, 0.5)
+        else:
+            u = oracle.thresholds(rule, seed, layer, t, 0, n, block) / TWO24
+        count += u < 1 - f
+    return -(count - T * (1 - f))
+
+
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl", "philox"])
+def test_proposition1_through_the_kernel(ssmq, rule):
+    """fp16 Mamba-1 rows, A = 0 (a = exp(0) = 1) and a constant write w = f s per
+    column: the GPU's stored state after T steps is h_0 + T w + e_T with e_T of
+    Proposition 1, exactly, for every rule."""
     import paper_2609_39185_amd as m
     n, T = 64, 300
     f_num = np.arange(1, n + 1) * 127
-    s = 2.0 ** -10
-    w = (f_num / 8192 * s).astype(np.float32)
-    st = torch.full((1, 1, 1, n), 0x3C00, dtype=torch.int16, device=DEV)
+    s = 2.0 ** -10                      # fp16 step in [1, 2)
+    f = f_num / 8192
+    w = (f * s).astype(np.float32)
+    st = torch.full((1, 1, 1, n), 0x3C00, dtype=torch.int16, device=DEV)  # 1.0
     one = torch.ones((1, 1, 1), device=DEV)
     A = torch.zeros((1, n), device=DEV)
     B = torch.from_numpy(w).reshape(1, 1, n).to(DEV)
     C = torch.zeros((1, 1, n), device=DEV)
     y = torch.empty((1, 1, 1), device=DEV)
-    thr = torch.empty(n, dtype=torch.int32, device=DEV)
-    count = np.zeros(n, np.int64)
+    say(f"case proposition 1 fp16 {rule}: {n} entries, {T} steps")
     for t in range(1, T + 1):
         m.state_update(st, None, one, torch.ones((1, 1), device=DEV), A, B, C, None, y,
-                       rule="weyl", fmt="fp16", step=t)
-        m.dither_fill(thr, rule="weyl", step=t)
-        torch.cuda.synchronize()
-        u = thr.cpu().numpy().view(np.uint32) / TWO24
-        count += u < 1 - f_num / 8192
+                       rule=rule, fmt="fp16", dither_block=16, seed=3, layer=1, step=t)
+    torch.cuda.synchronize()
     h = oracle.decode("fp16", wl.to_numpy_codes("fp16", st).ravel())
-    e_T = h - (1.0 + T * w.astype(np.float64))
-    assert np.allclose(e_T, -s * (count - T * (1 - f_num / 8192)), rtol=0, atol=1e-12)
+    e_T = (h - (1.0 + T * w.astype(np.float64))) / s
+    want = _prop1_prediction(rule, f, T, 3, 1, 16, n)
+    assert np.array_equal(e_T, want), (rule, np.nonzero(e_T != want)[0][:8])
+    if rule == "rtn":  # Corollary 1 (a): below half a step every write is erased
+        assert np.all(want == np.where(f < 0.5, -T * f, T * (1 - f)))
+
+
+@pytest.mark.parametrize("rule", ["rtn", "sr", "weyl", "philox"])
+def test_proposition1_through_the_kernel_e4m3_head(ssmq, rule):
+    """E4M3 with one scale per 64 x 128 head (the slab kernel the bench times).
+    Entry (0, 0) holds 448 and receives no write, so every step's scale is
+    448 / 448 = 1 exactly and every product is exact. Columns n >= 1 start at 1.0
+    and receive w = f/8, f = 3n / 8192 of the E4M3 step 1/8 in [1, 2), for T = 48
+    steps. An entry's stored value after t steps is 1 + N_up(t)/8 (N_up: the writes
+    that rounded up), so it stays in that binade, where Proposition 1 holds with one
+    fixed step, exactly while N_up(T) <= 7; those entries (all but a few SR draws)
+    follow Proposition 1 exactly, and column 0 stays where it started."""
+    import paper_2609_39185_amd as m
+    P, N, T = 64, 128, 48
+    f = 3.0 * np.arange(N) / 8192
+    codes = torch.full((1, 1, P, N), 0x38, dtype=torch.uint8)   # 1.0
+    codes[0, 0, 0, 0] = 0x7E                                      # 448
+    st = codes.to(DEV)
+    sc = torch.ones(1, device=DEV)
+    x = torch.ones((1, 1, P), device=DEV)
+    dt = torch.ones((1, 1), device=DEV)
+    A = torch.zeros(1, device=DEV)
+    B = torch.from_numpy((f / 8).astype(np.float32)).reshape(1, 1, N).to(DEV)
+    C = torch.zeros((1, 1, N), device=DEV)
+    y = torch.empty((1, 1, P), device=DEV)
+    say(f"case proposition 1 e4m3 head {rule}: {P * N} entries, {T} steps")
+    for t in range(1, T + 1):
+        m.state_update(st, sc, x, dt, A, B, C, None, y, rule=rule, fmt="e4m3", dither_block=128,
+                       seed=5, layer=2, step=t)
+    torch.cuda.synchronize()
+    assert sc.item() == 1.0
+    h = oracle.decode("e4m3", wl.to_numpy_codes("e4m3", st).ravel()).reshape(P, N)
+    assert h[0, 0] == 448.0 and np.all(h[1:, 0] == 1.0)
+    e_T = ((h - (1.0 + T * f / 8)) * 8)[:, 1:].ravel()
+    ff = np.tile(f[1:], P)
+    want = _prop1_prediction(rule, np.tile(f, P), T, 5, 2, 128, P * N).reshape(P, N)[:, 1:].ravel()
+    n_up = np.rint(want + T * ff).astype(np.int64)       # N_up(T) = e_T + T f
+    inside = n_up <= 7
+    say(f"  {int(inside.sum())} of {inside.size} entries stay in [1, 2)")
+    assert inside.mean() > 0.99
+    assert np.array_equal(e_T[inside], want[inside]), (rule, np.nonzero(e_T[inside] != want[inside])[0][:8])
+    if rule == "rtn":
+        assert np.all(want == -T * ff)
 
 
 # --------------------------------------------------------------------------
