@@ -364,6 +364,7 @@ def main() -> int:
         "cpu_baseline": cpu,
         "stream_ceiling": ceiling,
         "variants": results,
+        "targets": targets_summary(results),
         "configs": configs,
     }
     print(json.dumps(line), flush=True)
@@ -698,6 +699,26 @@ def state_error_study(w, *, steps: int, layers: int, block: int, device, fmt: st
 
 
 SWEEP_WORKLOADS = ("m1_small", "m2_ssd_b8", "m2_b64_fp8", "m1_long")
+TARGET_FRACTION = 0.80  # of peak HBM bandwidth, on the largest workload, per stored format
+
+
+def targets_summary(results: dict) -> dict:
+    """Each format's Weyl variant against the 80 % target, with what bounds it:
+    bf16 (4 B per entry) is bound by HBM; E4M3, INT8 and INT4 (2, 2 and 1 B per
+    entry) need two to four times the entries per second for the same bytes and
+    are bound by vector issue (the dithered conversion, threshold and sign per
+    entry)."""
+    out = {}
+    for key, r in results.items():
+        stored, rule = key.split(":", 1)
+        if rule != "weyl":
+            continue
+        fmt = stored.split("/")[0]
+        frac = r["pct_of_peak"] / 100.0
+        out[key] = {"pct_of_peak": r["pct_of_peak"], "target_pct": 100.0 * TARGET_FRACTION,
+                    "meets_target": frac >= TARGET_FRACTION,
+                    "bound": "hbm" if fmt in ("bf16", "fp16") else "vector issue"}
+    return out
 
 
 def graph_launch_us(w, fmt, rule, group, L, steps, warmup, device, t0=1):

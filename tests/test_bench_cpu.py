@@ -98,3 +98,14 @@ def test_variant_specs_and_their_algorithmic_bytes():
     assert bench.state_bytes_per_launch(w, "bf16") == 4 * n
     with pytest.raises(SystemExit):
         bench.parse_variant("bf16/128:weyl", w)
+
+
+def test_targets_summary_marks_each_format_against_80_percent():
+    import bench
+    res = {"bf16:weyl": {"pct_of_peak": 80.9}, "bf16:sr": {"pct_of_peak": 81.0},
+           "e4m3:weyl": {"pct_of_peak": 63.9}, "int8/128:weyl": {"pct_of_peak": 58.5}}
+    t = bench.targets_summary(res)
+    assert set(t) == {"bf16:weyl", "e4m3:weyl", "int8/128:weyl"}
+    assert t["bf16:weyl"]["meets_target"] and t["bf16:weyl"]["bound"] == "hbm"
+    assert not t["e4m3:weyl"]["meets_target"] and t["e4m3:weyl"]["bound"] == "vector issue"
+    assert t["int8/128:weyl"]["target_pct"] == 80.0
