@@ -895,6 +895,14 @@ def _csv_rows(d: str, suffix: str):
         return list(csv.DictReader(f))
 
 
+def _grid(row) -> int:
+    """Threads of a dispatch: the counter CSV has Grid_Size, the kernel trace CSV
+    Grid_Size_X, _Y and _Z."""
+    if row.get("Grid_Size") not in (None, ""):
+        return int(row["Grid_Size"])
+    return int(row["Grid_Size_X"]) * int(row["Grid_Size_Y"]) * int(row["Grid_Size_Z"])
+
+
 def _variant_of(kernel_name: str):
     import re
 
@@ -923,17 +931,17 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
 
     w = wl.WORKLOADS[workload]
     os.makedirs(PROFILE_DIR, exist_ok=True)
-    stats = _csv_rows(trace_dir, "kernel_stats.csv")
     trace = _csv_rows(trace_dir, "kernel_trace.csv")
     dur = defaultdict(list)
     for r in trace:
-        dur[r["Kernel_Name"]].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+        dur[(r["Kernel_Name"], _grid(r))].append(
+            int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
 
     def counter(d, name):
         vals = defaultdict(list)
         for r in _csv_rows(d, "counter_collection.csv"):
             if r["Counter_Name"] == name:
-                vals[(r["Kernel_Name"], int(r["Grid_Size"]))].append(float(r["Counter_Value"]))
+                vals[(r["Kernel_Name"], _grid(r))].append(float(r["Counter_Value"]))
         return vals
 
     fetch, write = counter(fetch_dir, "FETCH_SIZE"), counter(write_dir, "WRITE_SIZE")
@@ -961,7 +969,7 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
             "dispatches": len(v), "fetch_KiB": fk, "write_KiB": wk,
             "traffic_bytes": traffic, "algorithmic_bytes": algo,
             "traffic_over_algorithmic": traffic / algo,
-            "trace_avg_us": statistics.mean(dur[k]) / 1e3 if k in dur else None,
+            "trace_avg_us": statistics.mean(dur[(k, g)]) / 1e3 if (k, g) in dur else None,
         }
     rec = {
         "workload": workload,
@@ -989,17 +997,26 @@ def summarize_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir:
     with open(os.path.join(PROFILE_DIR, f"k_update_slab.{workload}.traffic.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
+    # Per (kernel, grid size): the default run also launches the same kernel
+    # instances on the smaller workloads of its configs block, whose launches
+    # must not be averaged with the hybrid stack's.
+    by_grid = defaultdict(list)
+    for r in trace:
+        by_grid[(r["Kernel_Name"], _grid(r))].append(
+            int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
     lines = [f"# Kernel trace of the default bench run on {workload}", "",
              "Command (repository root as $R, an output directory as $OUT, run from /tmp with TMPDIR=/tmp):", "",
              f"    {PROFILE_COMMANDS['trace']}", "",
-             "| kernel | calls | avg us | min us | max us | total ms |", "|---|---|---|---|---|---|"]
-    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:16]:
-        name = r["Name"]
+             "Launches grouped by kernel and grid size (threads); the largest grids are the "
+             f"{workload} layers, the smaller ones the configs block's workloads. The 16 kernels "
+             "with the most total time:", "",
+             "| kernel | grid | calls | avg us | min us | max us | total ms |",
+             "|---|---|---|---|---|---|---|"]
+    for (name, grid), v in sorted(by_grid.items(), key=lambda kv: -sum(kv[1]))[:16]:
         if len(name) > 80:
             name = name[:77] + "..."
-        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
-                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
-                     f"{float(r['TotalDurationNs']) / 1e6:.2f} |")
+        lines.append(f"| `{name}` | {grid} | {len(v)} | {statistics.mean(v) / 1e3:.1f} | "
+                     f"{min(v) / 1e3:.1f} | {max(v) / 1e3:.1f} | {sum(v) / 1e6:.2f} |")
     with open(os.path.join(PROFILE_DIR, f"k_update_slab.{workload}.kernel_trace.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps({k: round(v["traffic_over_algorithmic"], 4) for k, v in variants.items()}))
@@ -1114,16 +1131,16 @@ PROFILE_COMMANDS = {
              "-o run -- python3 $R/bench.py",
     "fetch": "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv "
              "-d $OUT/prof_fetch -o run -- python3 $R/bench.py --steps 2 --warmup 1 "
-             "--cpu-seconds 0",
+             "--cpu-seconds 0 --no-configs",
     "write": "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv "
              "-d $OUT/prof_write -o run -- python3 $R/bench.py --steps 2 --warmup 1 "
-             "--cpu-seconds 0",
+             "--cpu-seconds 0 --no-configs",
     "summary": "python3 $R/bench.py --summarize-profiles $OUT/prof_trace "
                "$OUT/prof_fetch $OUT/prof_write",
     "valu": "timeout -s KILL 120 rocprofv3 --pmc SQ_WAVES SQ_ACTIVE_INST_VALU SQ_WAVE_CYCLES "
             "SQ_BUSY_CYCLES SQ_INSTS_VALU GRBM_GUI_ACTIVE --output-format csv "
             "-d $OUT/pmc_busy -o run -- python3 $R/bench.py --steps 2 --warmup 0 "
-            "--layers 4 --cpu-seconds 0 --no-ceiling",
+            "--layers 4 --cpu-seconds 0 --no-ceiling --no-configs",
     "valu_summary": "python3 $R/bench.py --summarize-valu $OUT/pmc_busy",
     "replay_trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/prof_replay "
                     "-o run -- python3 $R/bench.py --replay --steps 4096",

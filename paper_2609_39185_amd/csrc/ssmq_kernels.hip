@@ -141,8 +141,10 @@ void k_update_slab(UpdateArgs a) {
   float h[CPT][V];
   bool bad[CPT];  // a NaN or infinity reached this chunk's partial of y
   float yo[CPT];  // rows' y, for kernels that store it directly
-  // Scaled formats store v * s_old; dA * (v * s_old) is evaluated as
-  // fma(fl32(dA * s_old), v, w). E4M3, and the four-chunk configurations (one
+  // Scaled formats store fl32(v * s_old); dA * h_prev is evaluated as
+  // fma(fl32(dA * s_old), v, w), one rounding of the scaled decay per group in
+  // place of one rounding of v * s_old per entry (it saves a multiply per entry;
+  // h_new moves by about an ulp at most). E4M3, and the four-chunk configurations (one
   // scale per head), read their scales before the loop (read inside it, each
   // load is issued after the previous chunk's y store and waited for at once);
   // the block-scaled INT kernels measure faster with one select-addressed load

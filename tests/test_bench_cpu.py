@@ -37,9 +37,14 @@ def test_profile_summary_scales_counters_by_the_calibration_kernel(tmp_path, mon
     _write_csv(str(trace / "run_kernel_stats.csv"),
                [{"Name": upd, "Calls": 2, "TotalDurationNs": 340000, "AverageNs": 170000,
                  "MinNs": 169000, "MaxNs": 171000}])
+    # two launches on the hybrid stack's grid, one of the same kernel on a smaller
+    # workload's grid (the configs block), which must not enter the average
+    g = {"Grid_Size_X": 1 << 20, "Grid_Size_Y": 1, "Grid_Size_Z": 1}
     _write_csv(str(trace / "run_kernel_trace.csv"),
-               [{"Kernel_Name": upd, "Start_Timestamp": 0, "End_Timestamp": 170000},
-                {"Kernel_Name": upd, "Start_Timestamp": 500000, "End_Timestamp": 670000}])
+               [{"Kernel_Name": upd, "Start_Timestamp": 0, "End_Timestamp": 170000, **g},
+                {"Kernel_Name": upd, "Start_Timestamp": 500000, "End_Timestamp": 670000, **g},
+                {"Kernel_Name": upd, "Start_Timestamp": 900000, "End_Timestamp": 906000,
+                 "Grid_Size_X": 1 << 14, "Grid_Size_Y": 1, "Grid_Size_Z": 1}])
     from paper_2609_39185_amd import workloads as wl
     algo = wl.WORKLOADS["hybrid_m2_stack"].entries_per_layer * 4
     for name, counter, cal_read, upd_read in (("fetch", "FETCH_SIZE", cal_kib / 2, algo / 2048.0),
