@@ -8,8 +8,9 @@ sequences" and the hash-SR unit-test moments (Appendix B "Decode regime"). The
 rest rests on mathematics: the decimal constants times 2^32 (Appendix B
 "Dithers"), the golden increment and Knuth's constant 2654435761 (Section 6.4
 "Three silent pitfalls"), the closed form of the fractional parts of t alpha,
-the correlation 1 - 6 d (1 - d) of two rotated streams, and the Philox4x32-10
-known answers of its authors.
+the correlation 1 - 6 d (1 - d) of two rotated streams, the Philox4x32-10
+known answers of its authors, and the MurmurHash3 known answers, which pin the
+fmix32 finalizer of the hash SR.
 """
 from decimal import Decimal, getcontext
 
@@ -208,6 +209,80 @@ def test_sr_keys_differ_by_seed_layer_step(orc):
         assert np.mean(base == other) < 0.01
     # a step's thresholds over entries are a bijection of the entry index (no repeats)
     assert len(np.unique(orc.thresholds("sr", 0, 0, 9, 0, 1 << 16, 16))) > (1 << 16) - 200
+
+
+# MurmurHash3_x86_32 (Appleby, SMHasher) ends in the 32-bit finalizer fmix32 that
+# the hash SR uses. Its published known answers, (bytes, seed) -> hash, pin the
+# oracle's finalizer: the body and tail below are the hash's published
+# definition, and every value passes through the oracle's fmix32 at the end.
+MURMUR3_KAT = [
+    (b"", 0, 0x00000000), (b"", 1, 0x514E28B7), (b"", 0xFFFFFFFF, 0x81F16F39),
+    (b"\xff\xff\xff\xff", 0, 0x76293B50), (b"!Ce\x87", 0, 0xF55B516B),
+    (b"!Ce\x87", 0x5082EDEE, 0x2362F9DE), (b"!Ce", 0, 0x7E4A8634), (b"!C", 0, 0xA0F7B07A),
+    (b"!", 0, 0x72661CF4), (b"\0\0\0\0", 0, 0x2362F9DE), (b"\0\0\0", 0, 0x85F0B427),
+    (b"\0\0", 0, 0x30F4C306), (b"\0", 0, 0x514E28B7), (b"aaaa", 0x9747B28C, 0x5A97808A),
+    (b"Hello, world!", 0x9747B28C, 0x24884CBA),
+    (b"The quick brown fox jumps over the lazy dog", 0x9747B28C, 0x2FA826CD),
+]
+
+
+def _murmur3_x86_32(data: bytes, seed: int, fmix) -> int:
+    m32 = 0xFFFFFFFF
+
+    def rotl(x, r):
+        return ((x << r) | (x >> (32 - r))) & m32
+
+    def scramble(k):
+        return (rotl((k * 0xCC9E2D51) & m32, 15) * 0x1B873593) & m32
+
+    h = seed & m32
+    whole = len(data) // 4
+    for i in range(whole):
+        h ^= scramble(int.from_bytes(data[4 * i:4 * i + 4], "little"))
+        h = (rotl(h, 13) * 5 + 0xE6546B64) & m32
+    tail = data[4 * whole:]
+    if tail:
+        h ^= scramble(int.from_bytes(tail, "little"))
+    return fmix(h ^ len(data))
+
+
+@pytest.mark.parametrize("data,seed,want", MURMUR3_KAT)
+def test_fmix32_through_murmur3_known_answers(orc, data, seed, want):
+    assert _murmur3_x86_32(data, seed, orc.fmix32) == want
+
+
+def test_sr_threshold_is_the_top_24_bits_of_fmix32(orc):
+    """Hash SR (Appendix B "Decode regime"): u = fmix32(i 0x9E3779B1 + key) truncated
+    to 24 bits, the key a per-(seed, layer, step) value; with the finalizer pinned
+    above, the entry term is checked here: consecutive entries' pre-images differ by
+    the paper's entry multiplier."""
+    for x in (0, 1, 0x80000000, 0xDEADBEEF, 0xFFFFFFFF):
+        assert _fmix32_inverse(orc.fmix32(x)) == x
+    seed, layer, t, base = 3, 11, 12345, 2 ** 33 + 5
+    got = orc.thresholds("sr", seed, layer, t, base, 8, 16)
+    # a threshold keeps 24 of the hash's 32 bits: each entry's pre-image is one of
+    # 256 values, and some choice for entry 0 must continue through all eight
+    # entries in steps of 0x9E3779B1 (a chance fit has probability about 2^-160)
+    pre = [{_fmix32_inverse((int(g) << 8) | lo) for lo in range(256)} for g in got]
+    assert any(all(((p0 + k * 0x9E3779B1) & 0xFFFFFFFF) in pre[k] for k in range(1, 8))
+               for p0 in pre[0])
+
+
+def _fmix32_inverse(h: int) -> int:
+    """Inverse of the MurmurHash3 finalizer (each xor-shift and odd multiply undone)."""
+    m32 = 0xFFFFFFFF
+
+    def unxorshift(x, s):
+        y = x
+        for _ in range(32 // s + 1):
+            y = x ^ (y >> s)
+        return y & m32
+
+    h = unxorshift(h, 16)
+    h = (h * pow(0xC2B2AE35, -1, 1 << 32)) & m32
+    h = unxorshift(h, 13)
+    h = (h * pow(0x85EBCA6B, -1, 1 << 32)) & m32
+    return unxorshift(h, 16)
 
 
 def test_rtn_nominal_threshold(orc):
