@@ -79,6 +79,18 @@ def test_step_head_tile_int(ssmq, fmt, rule, q):
     check_step(fmt, rule, *M2_SMALL, seed=30, what="int head tile", step=5, layer=2, **q)
 
 
+@pytest.mark.parametrize("fmt", ["int8", "int4", "e4m3"])
+@pytest.mark.parametrize("group", [32, 64, 256])
+@pytest.mark.parametrize("shape", [M2_SMALL, ("mamba2", 3, 6, 64, 64, 3)])
+def test_step_groups_of_several_lanes(ssmq, fmt, group, shape):
+    """Scale groups of 2, 4 and 16 lanes (16 entries per lane) in the head-slab
+    kernels, where neighbouring lanes split the scales of a pair of chunks between
+    them; rows of 128 and of 64 entries."""
+    for rule in ("rtn", "weyl"):
+        check_step(fmt, rule, *shape, seed=60 + group, what=f"{fmt} group {group} {shape}",
+                   scale_group=group, dither_block=128, step=7, layer=3)
+
+
 @pytest.mark.parametrize("fmt", ["int8", "int4"])
 @pytest.mark.parametrize("shape", [("mamba1", 3, 200, 1, 16, 1), ("mamba1", 1, 1536, 1, 16, 1),
                                    ("mamba2", 3, 6, 64, 64, 3), ("mamba2", 2, 2, 64, 256, 2),
