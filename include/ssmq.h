@@ -19,6 +19,9 @@
  *   - All arguments are validated on the host before any HIP call. A rejected
  *     call returns a non-zero status, touches no memory and leaves a message
  *     for ssmq_last_error(). A failed kernel launch returns SSMQ_EDEVICE.
+ *   - A call with nothing to do (batch 0, or n / n_entries 0) checks its
+ *     scalar arguments, returns SSMQ_OK and launches nothing; its pointer
+ *     arguments are not read and may be NULL.
  *   - Tensors are contiguous and row-major, with the layouts given below.
  *   - Step, layer and seed arithmetic is modulo 2^32.
  *   - Calls on different streams that write the same memory race; the library

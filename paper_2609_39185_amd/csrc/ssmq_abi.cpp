@@ -138,17 +138,8 @@ ssmq_status ssmq_state_update_ex(const ssmq_dims* dims, const ssmq_qparams* q,
     return fail(SSMQ_EINVAL, "nheads %d is not a multiple of ngroups %d", d.nheads, d.ngroups);
   if (d.a_per_state != 0 && d.a_per_state != 1)
     return fail(SSMQ_EINVAL, "a_per_state must be 0 or 1");
-  if (!state || !x || !dt || !A || !B || !C || !y)
-    return fail(SSMQ_EINVAL, "state, x, dt, A, B, C and y must not be NULL");
   const bool scaled = is_scaled(q->format);  // E4M3, INT8, INT4: one fp32 scale per group
   const bool fp32_state = (q->flags & SSMQ_FLAG_FP32_STATE) != 0;
-  if (scaled && !state_scale && !fp32_state)
-    return fail(SSMQ_EINVAL, "E4M3, INT8 and INT4 need state_scale");
-  if (!aligned(state, 16) || !aligned(B, 16) || !aligned(C, 16) || (d.a_per_state && !aligned(A, 16)))
-    return fail(SSMQ_EALIGN, "state, B, C (and A[nheads][dstate]) must be 16-byte aligned");
-  if (!aligned(x, 4) || !aligned(dt, 4) || !aligned(A, 4) || !aligned(y, 4) ||
-      (D && !aligned(D, 4)) || (state_scale && !aligned(state_scale, 4)))
-    return fail(SSMQ_EALIGN, "fp32 arrays must be 4-byte aligned");
 
   const int V = chunk_entries(q->format);
   if (d.dstate % V != 0 || !is_pow2(d.dstate / V) || d.dstate / V > 64)
@@ -166,7 +157,16 @@ ssmq_status ssmq_state_update_ex(const ssmq_dims* dims, const ssmq_qparams* q,
       return fail(SSMQ_EINVAL, "scale_group %lld must be a multiple of 16 dividing headdim*dstate",
                   static_cast<long long>(group));
   }
-  if (n_total == 0) return ok();
+  if (n_total == 0) return ok();  // nothing to do: the pointers are not read
+  if (!state || !x || !dt || !A || !B || !C || !y)
+    return fail(SSMQ_EINVAL, "state, x, dt, A, B, C and y must not be NULL");
+  if (scaled && !state_scale && !fp32_state)
+    return fail(SSMQ_EINVAL, "E4M3, INT8 and INT4 need state_scale");
+  if (!aligned(state, 16) || !aligned(B, 16) || !aligned(C, 16) || (d.a_per_state && !aligned(A, 16)))
+    return fail(SSMQ_EALIGN, "state, B, C (and A[nheads][dstate]) must be 16-byte aligned");
+  if (!aligned(x, 4) || !aligned(dt, 4) || !aligned(A, 4) || !aligned(y, 4) ||
+      (D && !aligned(D, 4)) || (state_scale && !aligned(state_scale, 4)))
+    return fail(SSMQ_EALIGN, "fp32 arrays must be 4-byte aligned");
 
   ssmq::UpdateArgs a{};
   a.state = state; a.scale = state_scale; a.x = x; a.dt = dt; a.A = A; a.B = B; a.C = C;

@@ -100,9 +100,14 @@ def test_state_update_validation(lib):
     assert _update(lib, D(1, 4, 64, 1024, 2, 0), Q("weyl", "bf16")) == EUNSUPPORTED
     assert _update(lib, good, Q("weyl", "e4m3", scale_group=48), scale=FAKE) == EINVAL
     assert _update(lib, good, Q("weyl", "e4m3", scale_group=2048), scale=FAKE) == EUNSUPPORTED
-    # an empty batch is a valid no-op that never reaches the device
+    # an empty batch is a valid no-op that never reaches the device; its scalar
+    # arguments are still checked, its pointers are not read and may be NULL
     assert _update(lib, D(0, 4, 64, 128, 2, 0), Q("weyl", "bf16")) == 0
     assert L.ssmq_last_error() == b""
+    nulls = dict(state=None, x=None, dt=None, A=None, B=None, C=None, y=None)
+    assert _update(lib, D(0, 4, 64, 128, 2, 0), Q("weyl", "e4m3"), **nulls) == 0
+    assert _update(lib, D(0, 4, 64, 128, 3, 0), Q("weyl", "bf16"), **nulls) == EINVAL
+    assert _update(lib, D(0, 4, 64, 128, 2, 0), Q("weyl", "e4m3", scale_group=48), **nulls) == EINVAL
 
 
 def test_requantize_validation(lib):
