@@ -440,6 +440,32 @@ def test_full_size_ssd_decode(ssmq):
 # --------------------------------------------------------------------------
 # errors surface as exceptions, before any work is queued
 # --------------------------------------------------------------------------
+@pytest.mark.parametrize("fmt", ["bf16", "e4m3", "int4"])
+def test_empty_inputs_are_no_ops(ssmq, fmt):
+    """Empty torch tensors (data pointer 0) through every entry point: each call
+    returns without error and launches nothing."""
+    H, P, N = 4, 64, 128
+    per = 2 if fmt == "int4" else 1
+    st = torch.empty((0, H, P, N // per), dtype=wl.CODE_TORCH_DTYPE[fmt], device=DEV)
+    sc = torch.empty((0,), device=DEV) if fmt != "bf16" else None
+    x, y = torch.empty((0, H, P), device=DEV), torch.empty((0, H, P), device=DEV)
+    dt, BC = torch.empty((0, H), device=DEV), torch.empty((0, 2, N), device=DEV)
+    A, D = torch.zeros(H, device=DEV), torch.zeros(H, device=DEV)
+    ssmq.state_update(st, sc, x, dt, A, BC, BC, D, y, rule="weyl", fmt=fmt)
+    ssmq.state_update(st, sc, x, dt, A, BC, BC, D, y, rule="sr", fmt=fmt, dt_softplus=True)
+    ssmq.requantize(torch.empty(0, device=DEV), st.view(-1), sc, rule="weyl", fmt=fmt,
+                    scale_group=16)
+    ssmq.dither_fill(torch.empty(0, dtype=torch.int32, device=DEV), rule="weyl")
+    cs = torch.empty((0, 8, 4), device=DEV)
+    ssmq.conv1d_update(cs, torch.empty((0, 8), device=DEV), torch.zeros((8, 4), device=DEV),
+                       None, torch.empty((0, 8), device=DEV))
+    e = torch.empty((0,), dtype=torch.float64, device=DEV)
+    ssmq.replay(torch.empty(0, device=DEV), torch.empty((0, 0), device=DEV),
+                torch.empty((0, 0), device=DEV), e, rule="weyl", fmt=fmt,
+                scale_group=0 if fmt == "bf16" else 16)
+    torch.cuda.synchronize()
+
+
 def test_errors(ssmq):
     import paper_2609_39185_amd as m
     st = torch.zeros((1, 4, 64, 128), dtype=torch.int16, device=DEV)
