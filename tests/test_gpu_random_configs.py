@@ -42,7 +42,7 @@ def _config(i):
          "dither_seed": int(rng.integers(0, 2 ** 32)), "layer": int(rng.integers(0, 64)),
          "step": int(rng.integers(0, 2 ** 32)), "entry_base": 16 * int(rng.integers(0, 2 ** 20))}
     if fmt in SCALED:
-        groups = [g for g in (16, 64, 128, 256, 1024) if head % g == 0]
+        groups = [g for g in (16, 32, 64, 128, 256, 512, 1024) if head % g == 0]
         per_head_ok = head % 16 == 0 and (
             (head <= 1024 and head & (head - 1) == 0)
             or (family == "mamba2" and head in (4096, 8192, 16384)))
@@ -52,7 +52,7 @@ def _config(i):
     return fmt, rule, (family, batch, nheads, headdim, dstate, ngroups), q
 
 
-@pytest.mark.parametrize("i", range(48))
+@pytest.mark.parametrize("i", range(96))
 def test_random_config(ssmq, i):
     fmt, rule, shape, q = _config(i)
     check_step(fmt, rule, *shape, seed=int(5000 + i), what=f"random config {i}", **q)
