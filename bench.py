@@ -98,6 +98,9 @@ def parse_args():
     ap.add_argument("--summarize-valu", metavar="PMC_DIR",
                     help="turn a rocprofv3 --pmc run of SQ_WAVES, SQ_INSTS_VALU, "
                          "SQ_ACTIVE_INST_VALU and GRBM_GUI_ACTIVE into profiles/...valu.md")
+    ap.add_argument("--summarize-mix", nargs=2, metavar=("PMC_DIR_A", "PMC_DIR_B"),
+                    help="turn the two --pmc runs of the instruction-mix counters into "
+                         "profiles/...valu_mix.md")
     return ap.parse_args()
 
 
@@ -141,6 +144,8 @@ def main() -> int:
         return summarize_profiles(args.workload, *args.summarize_profiles)
     if args.summarize_valu:
         return summarize_valu(args.workload, args.summarize_valu)
+    if args.summarize_mix:
+        return summarize_mix(args.workload, *args.summarize_mix)
     if args.summarize_trace:
         return summarize_replay_trace(*args.summarize_trace)
     if args.summarize_entry_trace:
@@ -1126,6 +1131,62 @@ def summarize_valu(workload: str, pmc_dir: str) -> int:
     return 0
 
 
+MIX_COUNTERS_A = ("SQ_INSTS_VALU_FMA_F32", "SQ_INSTS_VALU_MUL_F32", "SQ_INSTS_VALU_ADD_F32",
+                  "SQ_INSTS_VALU_CVT", "SQ_INSTS_VALU_INT32", "SQ_INSTS_VALU_INT64")
+MIX_COUNTERS_B = ("SQ_INSTS_VALU_FMA_F64", "SQ_INSTS_VALU_ADD_F64", "SQ_INSTS_VALU_MUL_F64",
+                  "SQ_INSTS_VALU_TRANS_F32", "SQ_INSTS_SALU", "SQ_INSTS_LDS", "SQ_INSTS_BRANCH")
+
+
+def summarize_mix(workload: str, dir_a: str, dir_b: str) -> int:
+    """Write profiles/k_update_slab.<workload>.valu_mix.md: per variant, the VALU
+    instructions per wave by kind (fp32 FMA, multiply and add, conversions, 32- and
+    64-bit integer, fp64, transcendental), the rest of the VALU count (bitwise,
+    min/max/med3, moves, selects, compares, DPP and byte permutes), and the scalar,
+    LDS and branch instructions per wave. Two --pmc passes, each with SQ_WAVES."""
+    import statistics
+    from collections import defaultdict
+
+    vals = defaultdict(lambda: defaultdict(list))
+    for d in (dir_a, dir_b):
+        for r in _csv_rows(d, "counter_collection.csv"):
+            if _variant_of(r["Kernel_Name"]) is not None:
+                key = (r["Kernel_Name"], d)
+                vals[key][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    per_wave = defaultdict(dict)
+    for (k, d), c in vals.items():
+        waves = statistics.mean(c["SQ_WAVES"])
+        for n, v in c.items():
+            if n != "SQ_WAVES":
+                per_wave[k][n] = statistics.mean(v) / waves
+    fp64 = ("SQ_INSTS_VALU_FMA_F64", "SQ_INSTS_VALU_ADD_F64", "SQ_INSTS_VALU_MUL_F64")
+    head = ["FMA f32", "MUL f32", "ADD f32", "CVT", "INT32", "INT64", "f64", "TRANS f32", "rest",
+            "VALU", "SALU", "LDS", "branch"]
+    lines = [f"# k_update_slab on {workload}: VALU instructions per wave by kind", "",
+             "Commands (repository root as $R, an output directory as $OUT, run from /tmp with TMPDIR=/tmp):",
+             "", f"    {PROFILE_COMMANDS['mix_a']}", f"    {PROFILE_COMMANDS['mix_b']}",
+             f"    {PROFILE_COMMANDS['mix_summary']}", "",
+             "Per wave (counter / SQ_WAVES of its pass). \"rest\" is SQ_INSTS_VALU minus the kinds "
+             "counted: bitwise operations, min / max / med3, moves, selects, compares, DPP moves and "
+             "byte permutes.", "",
+             "| variant | kernel | " + " | ".join(head) + " |", "|---|---|" + "---|" * len(head)]
+    rows = []
+    for k, c in per_wave.items():
+        if "SQ_INSTS_VALU" not in c or "SQ_INSTS_SALU" not in c:
+            continue
+        kinds = [c[n] for n in MIX_COUNTERS_A] + [sum(c[n] for n in fp64), c["SQ_INSTS_VALU_TRANS_F32"]]
+        rest = c["SQ_INSTS_VALU"] - sum(kinds)
+        rows.append((_variant_of(k), _short_kernel(k),
+                     kinds + [rest, c["SQ_INSTS_VALU"], c["SQ_INSTS_SALU"], c["SQ_INSTS_LDS"],
+                              c["SQ_INSTS_BRANCH"]]))
+    for v, k, nums in sorted(rows):
+        lines.append(f"| {v} | `{k}` | " + " | ".join(f"{x:.1f}" for x in nums) + " |")
+    os.makedirs(PROFILE_DIR, exist_ok=True)
+    with open(os.path.join(PROFILE_DIR, f"k_update_slab.{workload}.valu_mix.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 PROFILE_COMMANDS = {
     "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/prof_trace "
              "-o run -- python3 $R/bench.py",
@@ -1142,6 +1203,14 @@ PROFILE_COMMANDS = {
             "-d $OUT/pmc_busy -o run -- python3 $R/bench.py --steps 2 --warmup 0 "
             "--layers 4 --cpu-seconds 0 --no-ceiling --no-configs",
     "valu_summary": "python3 $R/bench.py --summarize-valu $OUT/pmc_busy",
+    "mix_a": "timeout -s KILL 120 rocprofv3 --pmc SQ_WAVES SQ_INSTS_VALU "
+             + " ".join(MIX_COUNTERS_A) + " --output-format csv -d $OUT/pmc_mix_a -o run -- "
+             "python3 $R/bench.py --steps 2 --warmup 0 --layers 4 --cpu-seconds 0 --no-ceiling "
+             "--no-configs",
+    "mix_b": "timeout -s KILL 120 rocprofv3 --pmc SQ_WAVES " + " ".join(MIX_COUNTERS_B)
+             + " --output-format csv -d $OUT/pmc_mix_b -o run -- python3 $R/bench.py --steps 2 "
+             "--warmup 0 --layers 4 --cpu-seconds 0 --no-ceiling --no-configs",
+    "mix_summary": "python3 $R/bench.py --summarize-mix $OUT/pmc_mix_a $OUT/pmc_mix_b",
     "replay_trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/prof_replay "
                     "-o run -- python3 $R/bench.py --replay --steps 4096",
     "entry_trace": "rocprofv3 --kernel-trace --stats --output-format csv -d $OUT/prof_entry "

@@ -114,3 +114,30 @@ def test_targets_summary_marks_each_format_against_80_percent():
     assert t["bf16:weyl"]["meets_target"] and t["bf16:weyl"]["bound"] == "hbm"
     assert not t["e4m3:weyl"]["meets_target"] and t["e4m3:weyl"]["bound"] == "vector issue"
     assert t["int8/128:weyl"]["target_pct"] == 80.0
+
+
+def test_instruction_mix_summary_per_wave(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "PROFILE_DIR", str(tmp_path / "profiles"))
+    upd = "void ssmq::k_update_slab<2, 2, 128, 4, true>(ssmq::UpdateArgs)"
+    other = "void at::native::elementwise_kernel<128, 4>"
+    a = {"SQ_WAVES": 10, "SQ_INSTS_VALU": 7450, "SQ_INSTS_VALU_FMA_F32": 1295,
+         "SQ_INSTS_VALU_MUL_F32": 1437, "SQ_INSTS_VALU_ADD_F32": 161, "SQ_INSTS_VALU_CVT": 977,
+         "SQ_INSTS_VALU_INT32": 1101, "SQ_INSTS_VALU_INT64": 85}
+    b = {"SQ_WAVES": 20, "SQ_INSTS_VALU_FMA_F64": 130, "SQ_INSTS_VALU_ADD_F64": 0,
+         "SQ_INSTS_VALU_MUL_F64": 10, "SQ_INSTS_VALU_TRANS_F32": 10, "SQ_INSTS_SALU": 3184,
+         "SQ_INSTS_LDS": 490, "SQ_INSTS_BRANCH": 566}
+    for d, cs in (("a", a), ("b", b)):
+        rows = [{"Kernel_Name": upd, "Grid_Size": 1 << 22, "Counter_Name": n, "Counter_Value": v}
+                for n, v in cs.items()]
+        rows.append({"Kernel_Name": other, "Grid_Size": 64, "Counter_Name": "SQ_WAVES",
+                     "Counter_Value": 1})
+        _write_csv(str(tmp_path / d / "run_counter_collection.csv"), rows)
+    assert bench.summarize_mix("hybrid_m2_stack", str(tmp_path / "a"), str(tmp_path / "b")) == 0
+    text = open(tmp_path / "profiles" / "k_update_slab.hybrid_m2_stack.valu_mix.md").read()
+    row = [ln for ln in text.splitlines() if ln.startswith("| e4m3:weyl")][0]
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    # per wave of each pass: 745 VALU, of which 129.5 + 143.7 + 16.1 + 97.7 + 110.1 + 8.5
+    # + 7.0 (f64) + 0.5 (trans) are counted by kind and 231.9 are the rest
+    assert cells[2:] == ["129.5", "143.7", "16.1", "97.7", "110.1", "8.5", "7.0", "0.5", "231.9",
+                         "745.0", "159.2", "24.5", "28.3"]
+    assert "elementwise_kernel" not in text and "--summarize-mix" in text
