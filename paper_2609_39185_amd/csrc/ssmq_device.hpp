@@ -482,9 +482,12 @@ __device__ inline uint4 quantize_e4m3_chunk(const float (&h)[16], float r, const
   }
   bool rare = maybe_nan;
   if constexpr (R != kRTN) {
-    float mn = __builtin_fabsf(h[0]);
+    // Started from +infinity, the chain is eight v_min3 with |h| as source
+    // modifiers (from |h[0]| the compiler first canonicalises two values). A NaN in
+    // h is caught by maybe_nan: it reaches the row's y.
+    float mn = __builtin_inff();
 #pragma unroll
-    for (int k = 1; k < 16; ++k) mn = fminf(mn, __builtin_fabsf(h[k]));
+    for (int k = 0; k < 16; ++k) mn = fminf(mn, __builtin_fabsf(h[k]));
     rare = rare || !(mn * r >= 0x1p-10f);
   }
   if (__builtin_amdgcn_ballot_w64(rare) != 0) {
