@@ -23,6 +23,9 @@ def test_softplus_dt_and_gate(orc):
     h0, (x, dt_raw, A, B, C, D), bias, z = _inputs(3)
     dt_raw = (dt_raw * 10 - 3).astype(np.float32)          # raw step sizes, both signs
     dt_raw[0, 0] = 30.0                                     # above the softplus threshold
+    # softplus arguments v = dt + bias of 0.5, 5, 19.5 and 20.5 (both sides of 20)
+    for (b, h), v in (((0, 1), 0.5), ((0, 2), 5.0), ((1, 0), 19.5), ((1, 3), 20.5)):
+        dt_raw[b, h] = np.float32(v) - bias[h]
     v = (dt_raw + bias[None, :]).astype(np.float32)
     dt_eff = np.where(v > 20, v, np.logaddexp(0.0, v.astype(np.float64))).astype(np.float32)
     codes = h0.view(np.uint32)

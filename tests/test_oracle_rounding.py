@@ -132,9 +132,17 @@ def test_dither_rule_is_eq_dither_exactly(orc, fmt):
 
 @pytest.mark.parametrize("fmt", ["fp16", "bf16", "e4m3"])
 def test_rtn_is_nearest_even_exactly(orc, fmt):
+    """Random values, and exact midpoints between neighbouring values of the format
+    (ties: the reference rounds them to the even step count)."""
     rng = np.random.default_rng(99 + len(fmt))
     lo_e, hi_e = RANGES[fmt]
     x = _random_floats(rng, 6000, lo_e, hi_e)
+    vals, _ = orc.grid(fmt)
+    vals = vals[np.isfinite(vals)]
+    k = rng.integers(0, vals.size - 1, 500)
+    mids = ((vals[k] + vals[k + 1]) / 2).astype(np.float32)
+    assert np.array_equal(mids.astype(np.float64), (vals[k] + vals[k + 1]) / 2)  # exact in fp32
+    x = np.concatenate([x, mids])
     codes = orc.round_values(fmt, "rtn", x)
     got = orc.decode(fmt, codes)
     for xi, gi in zip(x, got):

@@ -12,8 +12,6 @@ The mutation tests build copies of the oracle with one mistake planted in the
 step (the old scale dropped, a neighbouring group's scale read, the decay and the
 old scale multiplied first) and check that the pins reject each of them.
 """
-import os
-import subprocess
 from fractions import Fraction
 
 import numpy as np
@@ -21,8 +19,9 @@ import pytest
 import torch
 
 import oracle
-from oracle import build_oracle
 from paper_2609_39185_amd import workloads as wl
+
+from ._mutants import build_mutant
 
 QMAX = {"e4m3": 448.0, "int8": 127.0, "int4": 7.0}
 SHAPES = {  # (family, batch, nheads, headdim, dstate, ngroups)
@@ -165,22 +164,9 @@ MUTANTS = {
 }
 
 
-def _build_mutant(tmp_path, edits):
-    src = open(build_oracle.SOURCE).read()
-    for old, new in edits:
-        assert src.count(old) == 1, old
-        src = src.replace(old, new)
-    c = os.path.join(tmp_path, "mutant.c")
-    so = os.path.join(tmp_path, "libmutant.so")
-    with open(c, "w") as fh:
-        fh.write(src)
-    subprocess.run(["gcc", *build_oracle.CFLAGS, "-o", so, c, "-lm"], check=True)
-    return so
-
-
 @pytest.mark.parametrize("mutant", sorted(MUTANTS))
 def test_pins_reject_planted_mistakes(tmp_path, mutant):
-    so = _build_mutant(str(tmp_path), MUTANTS[mutant])
+    so = build_mutant(str(tmp_path), MUTANTS[mutant])
     with oracle.using_library(so):
         if mutant == "decay times old scale first":
             # both orders are eq. (rec) within a few fp32 roundings: the float64
