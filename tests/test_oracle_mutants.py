@@ -87,6 +87,15 @@ MUTANTS = {
         [("const float *Bg = B + (b * ngroups + g) * dstate;",
           "const float *Bg = B + (b * ngroups) * dstate;")],
         [lambda o: t_step.test_fp32_step_is_the_recurrence(o, "mamba2", (2, 6, 8, 32, 2))]),
+    "E4M3: exponent bias 8": (
+        [("{8, 4, 3, 7, 0},", "{8, 4, 3, 8, 0},")],
+        [t_round.test_e4m3_value_set]),
+    "fp16: subnormals one binade low": (
+        [("v = ldexp((double)m, 1 - d->bias - d->mbits);", "v = ldexp((double)m, -d->bias - d->mbits);")],
+        [lambda o: t_round.test_16bit_value_sets(o, "fp16"), t_round.test_e4m3_value_set]),
+    "E4M3: 0x7E read as NaN": (
+        [("e == emax_field && m == (1u << d->mbits) - 1u", "e == emax_field && m >= (1u << d->mbits) - 2u")],
+        [t_round.test_e4m3_value_set]),
     "softplus: threshold applied below 20 as well": (
         [("if (v > 20.0f) return v;", "if (v > 0.0f) return v;")],
         [t_dec.test_softplus_dt_and_gate]),
