@@ -355,7 +355,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": head_fmt,
+        "dtype": "f32",  # the arithmetic of the step; the stored format is config["format"]
         "data": "synthetic",
         "config": {"workload": w.name, "family": w.family, "batch": b, "layers": L, "nheads": H,
                    "headdim": P, "dstate": N, "ngroups": G, "format": head_fmt,
