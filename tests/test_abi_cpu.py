@@ -176,3 +176,34 @@ def test_header_is_self_contained(tmp_path, lang, compiler, std):
                         "-fsyntax-only", "-I", os.path.dirname(HEADER), str(src)],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_last_error_is_per_thread(lib):
+    """Threads that fail with different arguments each read their own message."""
+    import threading
+
+    L = lib.library()
+    errors = []
+
+    def worker(bad_n, rounds=2000):
+        for _ in range(rounds):
+            st = L.ssmq_dither_fill(2, 0, 0, 0, 0, bad_n, 16, FAKE, None)
+            msg = L.ssmq_last_error()
+            if st != EINVAL or msg != b"n < 0":
+                errors.append((bad_n, st, msg))
+                return
+
+    def worker_block(rounds=2000):
+        for _ in range(rounds):
+            st = L.ssmq_dither_fill(2, 0, 0, 0, 0, 16, 3, FAKE, None)
+            if st != EINVAL or b"dither_block" not in L.ssmq_last_error():
+                errors.append(("block", st, L.ssmq_last_error()))
+                return
+
+    threads = [threading.Thread(target=worker, args=(-1,)), threading.Thread(target=worker_block),
+               threading.Thread(target=worker, args=(-5,)), threading.Thread(target=worker_block)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert errors == []
