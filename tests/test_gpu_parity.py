@@ -274,29 +274,36 @@ def test_small_mamba1_workload_64_steps(ssmq, rule):
 
 
 @pytest.mark.parametrize("rule", ["rtn", "sr", "weyl"])
-def test_e4m3_head_scales_64_steps(ssmq, rule):
-    """Mamba-2 heads of 64 x 128 in E4M3 with one scale per head: 64 teacher-forced
-    steps, each checked against the oracle from the state and scales the GPU holds
-    (so a one-off difference cannot compound), with the scales evolving from step to
-    step and the per-head clamp taken or skipped as they fall."""
+@pytest.mark.parametrize("fmt,group", [("e4m3", 0), ("bf16", None), ("int8", 128)])
+def test_head_shape_64_steps(ssmq, fmt, group, rule):
+    """Mamba-2 heads of 64 x 128 (E4M3 with one scale per head, bf16, INT8 with blocks
+    of 128): 64 teacher-forced steps, each checked against the oracle from the state
+    and scales the GPU holds (so a one-off difference cannot compound), with the
+    scales evolving from step to step (E4M3: the per-head clamp taken or skipped as
+    they fall)."""
     import paper_2609_39185_amd as m
     b, H, P, N, G = 2, 8, 64, 128, 2
     A, D = wl.layer_params("mamba2", H, N, 120)
-    codes, scale = wl.initial_state("e4m3", b, H, P, N, 121)
-    st, sc = codes.to(DEV), scale.to(DEV)
+    codes, scale = wl.initial_state(fmt, b, H, P, N, 121, group=group or 0)
+    st = codes.to(DEV)
+    sc = None if scale is None else scale.to(DEV)
     Ad, Dd = A.to(DEV), D.to(DEV)
-    bar = Bar("e4m3", f"e4m3 per head {rule}, 64 steps")
+    q = {} if group is None else {"scale_group": group}
+    bar = Bar(fmt, f"{fmt} heads {rule}, 64 steps")
     for t in range(1, 65):
         x, dt, B, C = wl.step_inputs(b, H, P, N, G, 1200 + t)
-        before, s_before = wl.to_numpy_codes("e4m3", st), sc.cpu().numpy()
+        before = wl.to_numpy_codes(fmt, st)
+        s_before = None if sc is None else sc.cpu().numpy()
         y = torch.empty((b, H, P), dtype=torch.float32, device=DEV)
         m.state_update(st, sc, x.to(DEV), dt.to(DEV), Ad, B.to(DEV), C.to(DEV), Dd, y,
-                       rule=rule, fmt="e4m3", dither_block=128, step=t, layer=3)
+                       rule=rule, fmt=fmt, dither_block=128, step=t, layer=3, **q)
         torch.cuda.synchronize()
         r_codes, r_scale, r_y, r_h = oracle.state_update(
-            "e4m3", rule, before, s_before, x.numpy(), dt.numpy(), A.numpy(), B.numpy(),
-            C.numpy(), D.numpy(), step=t, layer=3, block=128)
-        bar.codes(wl.to_numpy_codes("e4m3", st), r_codes).scales(sc.cpu().numpy(), r_scale)
+            fmt, rule, before, s_before, x.numpy(), dt.numpy(), A.numpy(), B.numpy(),
+            C.numpy(), D.numpy(), step=t, layer=3, block=128, group=group or 0)
+        bar.codes(wl.to_numpy_codes(fmt, st), r_codes)
+        if sc is not None:
+            bar.scales(sc.cpu().numpy(), r_scale)
         bar.y(y.cpu().numpy(), r_y, y_magnitude(C.numpy(), r_h, D.numpy(), x.numpy(), H // G))
     bar.check()
 
